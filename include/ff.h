@@ -1,0 +1,203 @@
+/*
+ * ff.h - C ABI of the FlashForward renderer-attention library (libff, gfx950).
+ *
+ * One renderer forward of FlashForward (arxiv 2609.32540, Sec. 3.1 and
+ * Eq. step-update) takes the current chunk at one denoising stage as input,
+ * reads clean anchor KV and the same-stage history of earlier chunks as
+ * memory, produces its output, and publishes its own K/V for later chunks at
+ * that stage.  This library implements the attention part of that forward on
+ * one GPU, in three steps:
+ *
+ *   ff_rope3d          3D (t, h, w) rotary position embedding of Q and K
+ *   ff_chunk_attention attention of the chunk's queries over
+ *                      [anchor KV | stage-matched history KV | the chunk itself]
+ *   ff_kv_publish      the chunk's K/V into the stage's history ring
+ *                      (B_k <- Tail_W(B_k u (i, K, V)))
+ * plus ff_anchor_set, which replaces a layer's anchor segment (the clean
+ * anchor KV window A_Gamma(i) of Sec. 3.1).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.  The caller owns all device memory and all streams.  The cache's
+ *   device storage is one caller-allocated buffer of ff_cache_bytes() bytes
+ *   (256-byte aligned); the handle holds host-side bookkeeping only and must
+ *   not outlive that buffer.  The library never allocates device memory and
+ *   never synchronises a stream.
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL = the null
+ *   stream).  Device work is enqueued on it and nothing else; ordering
+ *   between calls is the caller's stream order.  Bookkeeping (ring slots,
+ *   anchor frames) is updated on the host when a call is enqueued, so calls on
+ *   one cache must be issued in the order the algorithm runs them (for one
+ *   (stage, layer): attention of chunk i, then publish of chunk i), and calls
+ *   touching the same (stage, layer) ring on different streams need the
+ *   caller's own synchronisation.  A handle is not thread-safe.
+ * Tensors.  Q, K, V and the attention output are dense, contiguous
+ *   [tokens][heads][head_dim] arrays of the cache's dtype (token-major, as a
+ *   DiT produces them).  The tokens of a run of latent frames are ordered
+ *   frame, then grid row, then grid column.  Pointers are device pointers.
+ * Indices.  stage is 0 .. num_stages-1 (stage s is the paper's k = S - s; the
+ *   mapping is only a name), layer is 0 .. num_layers-1, chunk_index is the
+ *   renderer chunk i, covering latent frames [B_R i, B_R i + B_R).
+ * Errors.  Every call returns an ff_status.  Arguments and bookkeeping are
+ *   validated on the host before anything is enqueued; on any error no device
+ *   work is enqueued and the handle is unchanged.  ff_last_error() returns a
+ *   thread-local message for the last failing call.  FF_ERR_HIP reports a
+ *   launch error returned by the HIP runtime (hipGetLastError); device faults
+ *   surface on the caller's next synchronisation, as with any HIP kernel.
+ */
+#ifndef FF_H_
+#define FF_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FF_ABI_VERSION 1
+#define FF_MAX_RING_CHUNKS 8     /* W <= 8 */
+#define FF_MAX_ANCHOR_FRAMES 8   /* anchor frames per layer */
+#define FF_MAX_ROPE_FRAMES 16    /* frames per ff_rope3d call */
+
+typedef enum {
+  FF_OK = 0,
+  FF_ERR_INVALID_ARG = 1,  /* NULL pointer or meaningless value */
+  FF_ERR_SHAPE = 2,        /* sizes inconsistent with the cache descriptor */
+  FF_ERR_ORDER = 3,        /* chunk index out of order for the ring */
+  FF_ERR_RANGE = 4,        /* stage, layer or frame index out of range */
+  FF_ERR_UNSUPPORTED = 5,  /* head_dim / dtype / limit not supported */
+  FF_ERR_HIP = 6,          /* the HIP runtime reported an error */
+  FF_ERR_BUFFER = 7        /* device buffer too small or misaligned */
+} ff_status;
+
+typedef enum { FF_DT_BF16 = 0, FF_DT_F32 = 1 } ff_dtype;
+
+/* Shape of one renderer cache: S stages x L layers of history rings of W
+ * chunks, plus one anchor segment per layer shared by all stages (the anchor
+ * KV is clean and carries no stage index, Sec. 3.1).
+ *   frames_per_chunk  B_R (3 in the paper)
+ *   grid_h, grid_w    latent tokens per frame = grid_h * grid_w
+ *   head_dim          64 or 128
+ *   rope_pairs_*      rotation pairs of the t, h and w axes; their sum must be
+ *                     head_dim / 2 (the Wan2.1 split is d/2 - 2*floor(d/6),
+ *                     floor(d/6), floor(d/6))
+ *   rope_theta        RoPE base (10000)
+ *   dtype             ff_dtype of every tensor and of the cache contents   */
+typedef struct {
+  int32_t num_stages;
+  int32_t num_layers;
+  int32_t ring_chunks;
+  int32_t frames_per_chunk;
+  int32_t grid_h;
+  int32_t grid_w;
+  int32_t num_heads;
+  int32_t head_dim;
+  int32_t max_anchor_frames;
+  int32_t rope_pairs_t;
+  int32_t rope_pairs_h;
+  int32_t rope_pairs_w;
+  double rope_theta;
+  int32_t dtype;
+  int32_t reserved;
+} ff_cache_desc;
+
+typedef struct ff_cache ff_cache; /* opaque host-side handle */
+
+/* ABI version of the loaded library (FF_ABI_VERSION). */
+int32_t ff_abi_version(void);
+
+/* Device bytes the cache described by `desc` needs; 0 if `desc` is invalid
+ * (ff_last_error() says why).  Layout: per layer an anchor segment of
+ * max_anchor_frames frames, per (stage, layer) W ring slots of one chunk each;
+ * every slot stores K and V head-major ([heads][tokens][head_dim]). */
+size_t ff_cache_bytes(const ff_cache_desc* desc);
+
+/* Create a handle over `dev_buf` (device memory of at least ff_cache_bytes()
+ * bytes, 256-byte aligned, owned by the caller).  Host-only: no device work.
+ * All rings start empty and no anchor segment is set. */
+ff_status ff_cache_create(const ff_cache_desc* desc, void* dev_buf, size_t dev_bytes,
+                          ff_cache** out);
+
+/* Free the host-side handle (device memory stays the caller's). NULL is a no-op. */
+ff_status ff_cache_destroy(ff_cache* cache);
+
+/* 3D RoPE, in place, on q and/or k (either may be NULL), each
+ * [n_frames * grid_h * grid_w][heads][head_dim] of the cache dtype.  Frame f of
+ * the run sits at latent time frame_t[f] (host array); a token's grid row and
+ * column are its h and w positions.  Pair p = (2p, 2p+1) is rotated by
+ * phi = pos_axis * theta^(-j / n_axis), where pairs [0, n_t) use t,
+ * [n_t, n_t + n_h) use the row and the rest the column, and j counts pairs
+ * inside the axis block: (a, b) -> (a cos phi - b sin phi, a sin phi + b cos phi).
+ * The paper fixes no RoPE; this is the convention of its Wan2.1 backbone.
+ * Rotation runs in float32 with angles from float64; bf16 results are
+ * rounded to nearest even.  1 <= n_frames <= FF_MAX_ROPE_FRAMES. */
+ff_status ff_rope3d(const ff_cache* cache, void* q, void* k, int32_t n_frames,
+                    const int32_t* frame_t, void* stream);
+
+/* Publish chunk `chunk_index`'s K and V ([B_R*grid_h*grid_w][heads][head_dim])
+ * into the history ring of (stage, layer): Eq. step-update,
+ * B_k <- Tail_W(B_k u (i, K, V)).  The chunk is copied bit for bit into slot
+ * chunk_index mod W, overwriting chunk_index - W.  The first publish of a ring
+ * may start at any chunk_index >= 0; every later one must be the previous
+ * one plus 1 (FF_ERR_ORDER otherwise).  Call it after ff_chunk_attention of
+ * the same chunk (read, evaluate, then write, as in the wavefront algorithm),
+ * since the slot it overwrites is one that attention still reads. */
+ff_status ff_kv_publish(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
+                        const void* k, const void* v, void* stream);
+
+/* Replace layer `layer`'s anchor segment, shared by every stage, with
+ * n_frames frames of clean anchor K (already rotated at its own frame
+ * positions) and V, each [n_frames*grid_h*grid_w][heads][head_dim].
+ * frame_t (host, n_frames values) records their latent positions for
+ * inspection; attention does not use them.  0 <= n_frames <= max_anchor_frames;
+ * n_frames = 0 clears the segment.  Copied bit for bit. */
+ff_status ff_anchor_set(ff_cache* cache, int32_t layer, int32_t n_frames, const int32_t* frame_t,
+                        const void* k, const void* v, void* stream);
+
+/* Renderer attention of chunk `chunk_index` at (stage, layer): every query of
+ * the chunk attends to
+ *   - every token of the layer's anchor segment (past and future anchors),
+ *   - every token of the ring's chunks max(0, i-W) .. i-1 (same stage only),
+ *   - every token of the chunk itself (k_cur, v_cur; bidirectional),
+ * out = softmax(softmax_scale * Q K^T) V per head (Sec. 3.1; the renderer row
+ * of the packed training mask with H = W).  q, k_cur, v_cur, out are
+ * [B_R*grid_h*grid_w][heads][head_dim].  The ring must hold exactly the chunks
+ * published before chunk_index (its next expected chunk equals chunk_index,
+ * or it is empty); FF_ERR_ORDER otherwise.  bf16: products on bf16 matrix
+ * cores with float32 accumulation, softmax in float32, probabilities and
+ * output rounded to bf16 (nearest even).  f32: float32 throughout.
+ * softmax_scale is normally 1/sqrt(head_dim). */
+ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
+                             const void* q, const void* k_cur, const void* v_cur, void* out,
+                             float softmax_scale, void* stream);
+
+/* Host bookkeeping of one ring: slot_chunk[s] (W entries, host) is the chunk
+ * held by slot s or -1; *published_count is the next chunk the ring expects
+ * (0 if nothing was published).  Either output may be NULL. */
+ff_status ff_cache_ring_state(const ff_cache* cache, int32_t stage, int32_t layer,
+                              int64_t* slot_chunk, int64_t* published_count);
+
+/* Anchor bookkeeping of one layer: *n_frames and frame_t[0 .. n_frames)
+ * (room for max_anchor_frames values).  Either output may be NULL. */
+ff_status ff_cache_anchor_state(const ff_cache* cache, int32_t layer, int32_t* n_frames,
+                                int32_t* frame_t);
+
+/* Copy cache contents out, on `stream`, in the logical [tokens][heads][head_dim]
+ * layout: stage >= 0 reads ring slot `slot` of (stage, layer) (one chunk);
+ * stage == -1 reads the layer's whole anchor segment (slot ignored;
+ * n_frames*grid_h*grid_w tokens).  k_out / v_out (device) may be NULL. */
+ff_status ff_cache_read(const ff_cache* cache, int32_t stage, int32_t layer, int32_t slot,
+                        void* k_out, void* v_out, void* stream);
+
+/* Name of a status code. */
+const char* ff_status_string(ff_status status);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* ff_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FF_H_ */

@@ -1,0 +1,96 @@
+// Float32 renderer attention (the fp32 workloads): one thread per query, key
+// tiles staged in LDS, online softmax in float32 with expf.  Small sizes
+// only; the bf16 kernel is the fast path.
+//
+// Launch shape: grid (ceil(nq / 128), heads), 128 threads.
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+
+#include "ff_internal.h"
+
+namespace ff {
+namespace {
+
+constexpr int kThreads = 128;
+constexpr int kTileK = 32;
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_f32_kernel(const float* __restrict__ q,
+                                                            float* __restrict__ out, int nq,
+                                                            int heads, float scale,
+                                                            KvSegments segs) {
+  __shared__ float ks[kTileK][D];
+  __shared__ float vs[kTileK][D];
+  const int head = blockIdx.y;
+  const int qi = blockIdx.x * kThreads + threadIdx.x;
+  const int qrow = min(qi, nq - 1);
+
+  float qv[D], o[D];
+  const float* qp = q + (int64_t(qrow) * heads + head) * D;
+#pragma unroll
+  for (int e = 0; e < D; ++e) {
+    qv[e] = qp[e] * scale;
+    o[e] = 0.0f;
+  }
+  float m = -INFINITY, l = 0.0f;
+
+  for (int sg = 0; sg < segs.n; ++sg) {
+    const KvSegment seg = segs.seg[sg];
+    const float* kb = static_cast<const float*>(seg.k) + head * seg.head_stride;
+    const float* vb = static_cast<const float*>(seg.v) + head * seg.head_stride;
+    for (int k0 = 0; k0 < seg.len; k0 += kTileK) {
+      const int n = min(kTileK, seg.len - k0);
+      __syncthreads();
+      for (int e = threadIdx.x; e < n * D; e += kThreads) {
+        const int r = e / D, c = e % D;
+        const int64_t off = int64_t(k0 + r) * seg.tok_stride + c;
+        ks[r][c] = kb[off];
+        vs[r][c] = vb[off];
+      }
+      __syncthreads();
+      for (int j = 0; j < n; ++j) {
+        float s = 0.0f;
+#pragma unroll
+        for (int e = 0; e < D; ++e) s = fmaf(qv[e], ks[j][e], s);
+        if (s > m) {
+          const float alpha = expf(m - s);
+          l *= alpha;
+#pragma unroll
+          for (int e = 0; e < D; ++e) o[e] *= alpha;
+          m = s;
+        }
+        const float p = expf(s - m);
+        l += p;
+#pragma unroll
+        for (int e = 0; e < D; ++e) o[e] = fmaf(p, vs[j][e], o[e]);
+      }
+    }
+  }
+  if (qi < nq) {
+    const float inv = 1.0f / l;
+    float* op = out + (int64_t(qi) * heads + head) * D;
+#pragma unroll
+    for (int e = 0; e < D; ++e) op[e] = o[e] * inv;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attention_f32(const void* q, void* out, int nq, int heads, int head_dim,
+                                float softmax_scale, const KvSegments& segs, hipStream_t stream) {
+  if (nq <= 0) return hipSuccess;
+  dim3 grid((nq + kThreads - 1) / kThreads, heads);
+  if (head_dim == 64)
+    hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(kThreads), 0, stream,
+                       static_cast<const float*>(q), static_cast<float*>(out), nq, heads,
+                       softmax_scale, segs);
+  else
+    hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(kThreads), 0, stream,
+                       static_cast<const float*>(q), static_cast<float*>(out), nq, heads,
+                       softmax_scale, segs);
+  return hipGetLastError();
+}
+
+}  // namespace ff

@@ -1,0 +1,411 @@
+// Host side of libff: descriptor validation, the device layout of the cache,
+// ring and anchor bookkeeping, the key-segment table of each attention call,
+// and the C ABI entry points declared in include/ff.h.
+//
+// The history ring of (stage, layer) realises the stage-matched renderer
+// history bank B_k of Sec. 3.1 (Eq. step-update): chunk c lives in slot
+// c mod W, and after publishing chunks c0 .. n-1 the valid slots hold exactly
+// Tail_W of that sequence.  The anchor segment of a layer is the clean anchor
+// KV window read by every stage.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "ff.h"
+#include "ff_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ff_status fail(ff_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+ff_status ok() {
+  g_last_error.clear();
+  return FF_OK;
+}
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+  size_t elem_bytes;
+  size_t tokens_per_frame;
+  size_t chunk_tokens;
+  size_t anchor_tokens;       // max_anchor_frames * tokens_per_frame
+  size_t anchor_tensor_bytes; // one of K / V of one layer's anchor segment
+  size_t slot_tensor_bytes;   // one of K / V of one ring slot
+  size_t anchor_base;         // offset of layer 0's anchor K
+  size_t ring_base;           // offset of (stage 0, layer 0, slot 0) K
+  size_t total;
+};
+
+ff_status check_desc(const ff_cache_desc* d) {
+  if (!d) return fail(FF_ERR_INVALID_ARG, "desc is NULL");
+  if (d->num_stages < 1 || d->num_layers < 1)
+    return fail(FF_ERR_INVALID_ARG, "num_stages and num_layers must be >= 1");
+  if (d->ring_chunks < 1 || d->ring_chunks > FF_MAX_RING_CHUNKS)
+    return fail(FF_ERR_UNSUPPORTED, "ring_chunks must be in [1, %d]", FF_MAX_RING_CHUNKS);
+  if (d->frames_per_chunk < 1 || d->frames_per_chunk > FF_MAX_ROPE_FRAMES)
+    return fail(FF_ERR_UNSUPPORTED, "frames_per_chunk must be in [1, %d]", FF_MAX_ROPE_FRAMES);
+  if (d->grid_h < 1 || d->grid_w < 1) return fail(FF_ERR_INVALID_ARG, "grid must be >= 1x1");
+  if (d->num_heads < 1) return fail(FF_ERR_INVALID_ARG, "num_heads must be >= 1");
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(FF_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (d->max_anchor_frames < 0 || d->max_anchor_frames > FF_MAX_ANCHOR_FRAMES)
+    return fail(FF_ERR_UNSUPPORTED, "max_anchor_frames must be in [0, %d]", FF_MAX_ANCHOR_FRAMES);
+  if (d->rope_pairs_t < 0 || d->rope_pairs_h < 0 || d->rope_pairs_w < 0 ||
+      d->rope_pairs_t + d->rope_pairs_h + d->rope_pairs_w != d->head_dim / 2)
+    return fail(FF_ERR_INVALID_ARG, "rope pairs must be >= 0 and sum to head_dim / 2");
+  if (!(d->rope_theta > 0.0) || !std::isfinite(d->rope_theta))
+    return fail(FF_ERR_INVALID_ARG, "rope_theta must be positive");
+  if (d->dtype != FF_DT_BF16 && d->dtype != FF_DT_F32)
+    return fail(FF_ERR_UNSUPPORTED, "dtype must be FF_DT_BF16 or FF_DT_F32");
+  const double tokens = double(d->grid_h) * d->grid_w * d->frames_per_chunk;
+  const double anchor_tokens = double(d->grid_h) * d->grid_w * d->max_anchor_frames;
+  if (tokens * d->num_heads * d->head_dim > 2.0e9 || anchor_tokens > 2.0e9 ||
+      tokens * (d->ring_chunks + 1) + anchor_tokens > 2.0e9)
+    return fail(FF_ERR_UNSUPPORTED, "chunk too large (element indices must fit in 32 bits)");
+  return FF_OK;
+}
+
+Layout make_layout(const ff_cache_desc* d) {
+  Layout L;
+  L.elem_bytes = d->dtype == FF_DT_BF16 ? 2 : 4;
+  L.tokens_per_frame = size_t(d->grid_h) * d->grid_w;
+  L.chunk_tokens = L.tokens_per_frame * d->frames_per_chunk;
+  L.anchor_tokens = L.tokens_per_frame * d->max_anchor_frames;
+  const size_t row = L.elem_bytes * d->head_dim;
+  L.anchor_tensor_bytes = align_up(L.anchor_tokens * d->num_heads * row);
+  L.slot_tensor_bytes = align_up(L.chunk_tokens * d->num_heads * row);
+  L.anchor_base = 0;
+  L.ring_base = L.anchor_base + 2 * L.anchor_tensor_bytes * d->num_layers;
+  L.total = L.ring_base +
+            2 * L.slot_tensor_bytes * size_t(d->ring_chunks) * d->num_layers * d->num_stages;
+  return L;
+}
+
+}  // namespace
+
+struct ff_cache {
+  ff_cache_desc desc;
+  Layout layout;
+  char* dev;  // caller-owned device buffer
+  // ring bookkeeping per (stage, layer): slot -> chunk (-1 empty), next chunk (-1 unset)
+  std::vector<int64_t> slot_chunk;
+  std::vector<int64_t> next_chunk;
+  // anchor bookkeeping per layer
+  std::vector<int32_t> anchor_frames;  // [layer][max_anchor_frames]
+  std::vector<int32_t> anchor_count;
+
+  size_t ring_index(int s, int l) const { return size_t(s) * desc.num_layers + l; }
+  char* anchor_k(int l) const { return dev + layout.anchor_base + 2 * layout.anchor_tensor_bytes * l; }
+  char* anchor_v(int l) const { return anchor_k(l) + layout.anchor_tensor_bytes; }
+  char* slot_k(int s, int l, int slot) const {
+    const size_t i = (ring_index(s, l) * desc.ring_chunks + slot) * 2;
+    return dev + layout.ring_base + i * layout.slot_tensor_bytes;
+  }
+  char* slot_v(int s, int l, int slot) const { return slot_k(s, l, slot) + layout.slot_tensor_bytes; }
+  int row_bytes() const { return int(layout.elem_bytes) * desc.head_dim; }
+};
+
+namespace {
+
+ff_status check_stage_layer(const ff_cache* c, int stage, int layer) {
+  if (stage < 0 || stage >= c->desc.num_stages)
+    return fail(FF_ERR_RANGE, "stage %d out of range [0, %d)", stage, c->desc.num_stages);
+  if (layer < 0 || layer >= c->desc.num_layers)
+    return fail(FF_ERR_RANGE, "layer %d out of range [0, %d)", layer, c->desc.num_layers);
+  return FF_OK;
+}
+
+// Kernels move 16-byte vectors: every tensor pointer must be 16-byte aligned.
+ff_status check_aligned(const void* p, const char* name) {
+  if (reinterpret_cast<uintptr_t>(p) % 16 != 0)
+    return fail(FF_ERR_INVALID_ARG, "%s must be 16-byte aligned", name);
+  return FF_OK;
+}
+
+ff_status hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(FF_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t ff_abi_version(void) { return FF_ABI_VERSION; }
+
+size_t ff_cache_bytes(const ff_cache_desc* desc) {
+  if (check_desc(desc) != FF_OK) return 0;
+  g_last_error.clear();
+  return make_layout(desc).total;
+}
+
+ff_status ff_cache_create(const ff_cache_desc* desc, void* dev_buf, size_t dev_bytes,
+                          ff_cache** out) {
+  if (!out) return fail(FF_ERR_INVALID_ARG, "out is NULL");
+  ff_status st = check_desc(desc);
+  if (st != FF_OK) return st;
+  if (!dev_buf) return fail(FF_ERR_INVALID_ARG, "dev_buf is NULL");
+  if (reinterpret_cast<uintptr_t>(dev_buf) % kAlign != 0)
+    return fail(FF_ERR_BUFFER, "dev_buf must be %zu-byte aligned", kAlign);
+  const Layout L = make_layout(desc);
+  if (dev_bytes < L.total)
+    return fail(FF_ERR_BUFFER, "dev_bytes %zu < required %zu", dev_bytes, L.total);
+  ff_cache* c = new (std::nothrow) ff_cache;
+  if (!c) return fail(FF_ERR_INVALID_ARG, "out of host memory");
+  c->desc = *desc;
+  c->layout = L;
+  c->dev = static_cast<char*>(dev_buf);
+  const size_t rings = size_t(desc->num_stages) * desc->num_layers;
+  c->slot_chunk.assign(rings * desc->ring_chunks, -1);
+  c->next_chunk.assign(rings, -1);
+  c->anchor_frames.assign(size_t(desc->num_layers) * (desc->max_anchor_frames + 1), 0);
+  c->anchor_count.assign(desc->num_layers, 0);
+  *out = c;
+  return ok();
+}
+
+ff_status ff_cache_destroy(ff_cache* cache) {
+  delete cache;
+  return ok();
+}
+
+ff_status ff_rope3d(const ff_cache* cache, void* q, void* k, int32_t n_frames,
+                    const int32_t* frame_t, void* stream) {
+  if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
+  if (!q && !k) return ok();
+  if (n_frames < 1 || n_frames > FF_MAX_ROPE_FRAMES)
+    return fail(FF_ERR_UNSUPPORTED, "n_frames must be in [1, %d]", FF_MAX_ROPE_FRAMES);
+  if (!frame_t) return fail(FF_ERR_INVALID_ARG, "frame_t is NULL");
+  if (check_aligned(q, "q") != FF_OK || check_aligned(k, "k") != FF_OK) return FF_ERR_INVALID_ARG;
+  const ff_cache_desc& d = cache->desc;
+  ff::RopeParams p;
+  std::memset(&p, 0, sizeof(p));
+  for (int f = 0; f < n_frames; ++f) {
+    if (frame_t[f] < 0) return fail(FF_ERR_RANGE, "frame_t[%d] = %d < 0", f, frame_t[f]);
+    p.frame_t[f] = frame_t[f];
+  }
+  p.n_t = d.rope_pairs_t;
+  p.n_th = d.rope_pairs_t + d.rope_pairs_h;
+  const int axis_n[3] = {d.rope_pairs_t, d.rope_pairs_h, d.rope_pairs_w};
+  int pair = 0;
+  for (int a = 0; a < 3; ++a)
+    for (int j = 0; j < axis_n[a]; ++j)
+      p.omega[pair++] = std::pow(d.rope_theta, -double(j) / double(axis_n[a]));
+  const int n_tok = n_frames * d.grid_h * d.grid_w;
+  hipError_t e = ff::launch_rope3d(q, k, n_tok, d.num_heads, d.head_dim, d.dtype, d.grid_w,
+                                   d.grid_h * d.grid_w, p, static_cast<hipStream_t>(stream));
+  return hip_status(e, "rope3d launch");
+}
+
+ff_status ff_kv_publish(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
+                        const void* k, const void* v, void* stream) {
+  if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
+  if (!k || !v) return fail(FF_ERR_INVALID_ARG, "k and v must be non-NULL");
+  if (check_aligned(k, "k") != FF_OK || check_aligned(v, "v") != FF_OK) return FF_ERR_INVALID_ARG;
+  ff_status st = check_stage_layer(cache, stage, layer);
+  if (st != FF_OK) return st;
+  if (chunk_index < 0) return fail(FF_ERR_RANGE, "chunk_index %lld < 0", (long long)chunk_index);
+  const size_t r = cache->ring_index(stage, layer);
+  const int64_t expected = cache->next_chunk[r];
+  if (expected >= 0 && chunk_index != expected)
+    return fail(FF_ERR_ORDER, "publish of chunk %lld at (stage %d, layer %d); the ring expects %lld",
+                (long long)chunk_index, stage, layer, (long long)expected);
+  const int W = cache->desc.ring_chunks;
+  const int slot = int(chunk_index % W);
+  const ff_cache_desc& d = cache->desc;
+  hipError_t e = ff::launch_kv_scatter(
+      k, v, cache->slot_k(stage, layer, slot), cache->slot_v(stage, layer, slot),
+      int(cache->layout.chunk_tokens), d.num_heads, cache->row_bytes(),
+      int64_t(cache->layout.chunk_tokens) * cache->row_bytes(), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_status(e, "kv_publish launch");
+  cache->slot_chunk[r * W + slot] = chunk_index;
+  cache->next_chunk[r] = chunk_index + 1;
+  return ok();
+}
+
+ff_status ff_anchor_set(ff_cache* cache, int32_t layer, int32_t n_frames, const int32_t* frame_t,
+                        const void* k, const void* v, void* stream) {
+  if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
+  const ff_cache_desc& d = cache->desc;
+  if (layer < 0 || layer >= d.num_layers)
+    return fail(FF_ERR_RANGE, "layer %d out of range [0, %d)", layer, d.num_layers);
+  if (n_frames < 0 || n_frames > d.max_anchor_frames)
+    return fail(FF_ERR_RANGE, "n_frames %d out of range [0, %d]", n_frames, d.max_anchor_frames);
+  if (n_frames > 0 && (!k || !v || !frame_t))
+    return fail(FF_ERR_INVALID_ARG, "k, v and frame_t must be non-NULL");
+  if (n_frames > 0 && (check_aligned(k, "k") != FF_OK || check_aligned(v, "v") != FF_OK))
+    return FF_ERR_INVALID_ARG;
+  if (n_frames > 0) {
+    const int n_tok = n_frames * d.grid_h * d.grid_w;
+    hipError_t e = ff::launch_kv_scatter(
+        k, v, cache->anchor_k(layer), cache->anchor_v(layer), n_tok, d.num_heads,
+        cache->row_bytes(), int64_t(cache->layout.anchor_tokens) * cache->row_bytes(),
+        static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_status(e, "anchor_set launch");
+  }
+  int32_t* fr = &cache->anchor_frames[size_t(layer) * (d.max_anchor_frames + 1)];
+  for (int f = 0; f < n_frames; ++f) fr[f] = frame_t[f];
+  cache->anchor_count[layer] = n_frames;
+  return ok();
+}
+
+ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
+                             const void* q, const void* k_cur, const void* v_cur, void* out,
+                             float softmax_scale, void* stream) {
+  if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
+  if (!q || !k_cur || !v_cur || !out)
+    return fail(FF_ERR_INVALID_ARG, "q, k_cur, v_cur and out must be non-NULL");
+  if (check_aligned(q, "q") != FF_OK || check_aligned(k_cur, "k_cur") != FF_OK ||
+      check_aligned(v_cur, "v_cur") != FF_OK || check_aligned(out, "out") != FF_OK)
+    return FF_ERR_INVALID_ARG;
+  ff_status st = check_stage_layer(cache, stage, layer);
+  if (st != FF_OK) return st;
+  if (chunk_index < 0) return fail(FF_ERR_RANGE, "chunk_index %lld < 0", (long long)chunk_index);
+  if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
+    return fail(FF_ERR_INVALID_ARG, "softmax_scale must be positive and finite");
+  const ff_cache_desc& d = cache->desc;
+  const size_t r = cache->ring_index(stage, layer);
+  const int64_t expected = cache->next_chunk[r];
+  if (expected >= 0 && chunk_index != expected)
+    return fail(FF_ERR_ORDER,
+                "attention of chunk %lld at (stage %d, layer %d); the ring holds chunks up to %lld",
+                (long long)chunk_index, stage, layer, (long long)(expected - 1));
+  const int W = d.ring_chunks;
+  const int heads = d.num_heads;
+  const int D = d.head_dim;
+  const int chunk_tokens = int(cache->layout.chunk_tokens);
+
+  ff::KvSegments segs;
+  std::memset(&segs, 0, sizeof(segs));
+  auto add = [&](const void* kp, const void* vp, int64_t head_stride, int tok_stride, int len) {
+    ff::KvSegment& s = segs.seg[segs.n++];
+    s.k = kp;
+    s.v = vp;
+    s.head_stride = head_stride;
+    s.tok_stride = tok_stride;
+    s.len = len;
+    segs.total += len;
+  };
+  // anchors: head-major, max_anchor_frames * G token stride per head
+  const int n_anchor = cache->anchor_count[layer];
+  if (n_anchor > 0)
+    add(cache->anchor_k(layer), cache->anchor_v(layer), int64_t(cache->layout.anchor_tokens) * D, D,
+        n_anchor * d.grid_h * d.grid_w);
+  // history: chunks max(0, i - W) .. i - 1 that the ring holds, in chunk order
+  for (int64_t c = chunk_index - W; c < chunk_index; ++c) {
+    if (c < 0) continue;
+    const int slot = int(c % W);
+    if (cache->slot_chunk[r * W + slot] != c) continue;
+    add(cache->slot_k(stage, layer, slot), cache->slot_v(stage, layer, slot),
+        int64_t(chunk_tokens) * D, D, chunk_tokens);
+  }
+  // the chunk itself: token-major
+  add(k_cur, v_cur, D, heads * D, chunk_tokens);
+
+  hipError_t e;
+  if (d.dtype == FF_DT_BF16)
+    e = ff::launch_attention_bf16(q, out, chunk_tokens, heads, D, softmax_scale, segs,
+                                  static_cast<hipStream_t>(stream));
+  else
+    e = ff::launch_attention_f32(q, out, chunk_tokens, heads, D, softmax_scale, segs,
+                                 static_cast<hipStream_t>(stream));
+  return hip_status(e, "chunk_attention launch");
+}
+
+ff_status ff_cache_ring_state(const ff_cache* cache, int32_t stage, int32_t layer,
+                              int64_t* slot_chunk, int64_t* published_count) {
+  if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
+  ff_status st = check_stage_layer(cache, stage, layer);
+  if (st != FF_OK) return st;
+  const size_t r = cache->ring_index(stage, layer);
+  const int W = cache->desc.ring_chunks;
+  if (slot_chunk)
+    for (int s = 0; s < W; ++s) slot_chunk[s] = cache->slot_chunk[r * W + s];
+  if (published_count) *published_count = cache->next_chunk[r] < 0 ? 0 : cache->next_chunk[r];
+  return ok();
+}
+
+ff_status ff_cache_anchor_state(const ff_cache* cache, int32_t layer, int32_t* n_frames,
+                                int32_t* frame_t) {
+  if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
+  const ff_cache_desc& d = cache->desc;
+  if (layer < 0 || layer >= d.num_layers)
+    return fail(FF_ERR_RANGE, "layer %d out of range [0, %d)", layer, d.num_layers);
+  const int n = cache->anchor_count[layer];
+  if (n_frames) *n_frames = n;
+  if (frame_t)
+    for (int f = 0; f < n; ++f) frame_t[f] = cache->anchor_frames[size_t(layer) * (d.max_anchor_frames + 1) + f];
+  return ok();
+}
+
+ff_status ff_cache_read(const ff_cache* cache, int32_t stage, int32_t layer, int32_t slot,
+                        void* k_out, void* v_out, void* stream) {
+  if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
+  const ff_cache_desc& d = cache->desc;
+  if (layer < 0 || layer >= d.num_layers)
+    return fail(FF_ERR_RANGE, "layer %d out of range [0, %d)", layer, d.num_layers);
+  if (!k_out && !v_out) return ok();
+  if (check_aligned(k_out, "k_out") != FF_OK || check_aligned(v_out, "v_out") != FF_OK)
+    return FF_ERR_INVALID_ARG;
+  const void *ks, *vs;
+  int n_tok;
+  int64_t head_stride_bytes;
+  if (stage == -1) {
+    n_tok = cache->anchor_count[layer] * d.grid_h * d.grid_w;
+    ks = cache->anchor_k(layer);
+    vs = cache->anchor_v(layer);
+    head_stride_bytes = int64_t(cache->layout.anchor_tokens) * cache->row_bytes();
+  } else {
+    ff_status st = check_stage_layer(cache, stage, layer);
+    if (st != FF_OK) return st;
+    if (slot < 0 || slot >= d.ring_chunks)
+      return fail(FF_ERR_RANGE, "slot %d out of range [0, %d)", slot, d.ring_chunks);
+    n_tok = int(cache->layout.chunk_tokens);
+    ks = cache->slot_k(stage, layer, slot);
+    vs = cache->slot_v(stage, layer, slot);
+    head_stride_bytes = int64_t(cache->layout.chunk_tokens) * cache->row_bytes();
+  }
+  if (n_tok == 0) return ok();
+  hipError_t e = ff::launch_kv_gather(k_out ? ks : nullptr, v_out ? vs : nullptr, k_out, v_out,
+                                      n_tok, d.num_heads, cache->row_bytes(), head_stride_bytes,
+                                      static_cast<hipStream_t>(stream));
+  return hip_status(e, "cache_read launch");
+}
+
+const char* ff_status_string(ff_status status) {
+  switch (status) {
+    case FF_OK: return "FF_OK";
+    case FF_ERR_INVALID_ARG: return "FF_ERR_INVALID_ARG";
+    case FF_ERR_SHAPE: return "FF_ERR_SHAPE";
+    case FF_ERR_ORDER: return "FF_ERR_ORDER";
+    case FF_ERR_RANGE: return "FF_ERR_RANGE";
+    case FF_ERR_UNSUPPORTED: return "FF_ERR_UNSUPPORTED";
+    case FF_ERR_HIP: return "FF_ERR_HIP";
+    case FF_ERR_BUFFER: return "FF_ERR_BUFFER";
+  }
+  return "FF_ERR_UNKNOWN";
+}
+
+const char* ff_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

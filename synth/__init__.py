@@ -56,7 +56,7 @@ class Workload:
     layers: int
     n_chunks: int                 # chunks generated in sequence
     input_scale: float
-    anchor_rule: str              # "fixed:<f0>,<f1>,..." | "window" | "every8"
+    anchor_rule: str              # "none" | "fixed:<f0>,<f1>,..." | "window" | "every8"
     max_anchor_frames: int
 
     @property
@@ -82,6 +82,8 @@ class Workload:
     def anchor_frames_for_chunk(self, i: int) -> List[int]:
         """Latent frame positions of the anchor segment visible to chunk i."""
         rule = self.anchor_rule
+        if rule == "none":
+            return []
         if rule.startswith("fixed:"):
             return [int(v) for v in rule[len("fixed:"):].split(",")]
         if rule == "window":

@@ -1,0 +1,134 @@
+"""The C ABI library loads, exports every entry point of include/ff.h, and its
+host-side validation behaves as documented.  No GPU: only calls that never
+reach a kernel launch are made (the device pointer is never dereferenced by
+them)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_32540_amd import ff
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ff.h")
+
+FAKE_DEV = 0x7f0000000000  # 256-byte aligned; only stored, never dereferenced here
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ff_[a-z0-9_]+)\s*\(", text)))
+
+
+def desc(**kw):
+    base = dict(num_stages=4, num_layers=2, ring_chunks=4, frames_per_chunk=3, grid_h=30,
+                grid_w=52, num_heads=12, head_dim=128, max_anchor_frames=3, rope_pairs_t=22,
+                rope_pairs_h=21, rope_pairs_w=21, rope_theta=10000.0, dtype=ff.FF_DT_BF16,
+                reserved=0)
+    base.update(kw)
+    return ff.CacheDesc(**base)
+
+
+def test_library_exports_every_header_symbol():
+    L = ff.lib()
+    names = header_functions()
+    assert len(names) == 13
+    for n in names:
+        assert hasattr(L, n), n
+    assert {n for n, _, _ in ff.SIGNATURES} == set(names)
+    assert L.ff_abi_version() == 1
+
+
+def test_cache_bytes_layout():
+    L = ff.lib()
+    d = desc()
+    # anchors: layers x 2 x (3 frames x 1560 tokens x 12 heads x 128 x 2 B)
+    # rings: stages x layers x W x 2 x (4680 x 12 x 128 x 2 B), all 256-aligned
+    anchor = 3 * 1560 * 12 * 128 * 2
+    slot = 4680 * 12 * 128 * 2
+    align = lambda x: (x + 255) // 256 * 256
+    assert L.ff_cache_bytes(ctypes.byref(d)) == 2 * 2 * align(anchor) + 4 * 2 * 4 * 2 * align(slot)
+    # C5-shaped, all 4 stages x 40 layers: ~150 GB fits one MI355X
+    d5 = desc(num_layers=40, grid_h=45, grid_w=80, num_heads=40)
+    assert 140e9 < L.ff_cache_bytes(ctypes.byref(d5)) < 160e9
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 96, 5), ("ring_chunks", 0, 5), ("ring_chunks", 9, 5), ("dtype", 7, 5),
+    ("rope_pairs_t", 21, 1), ("num_heads", 0, 1), ("max_anchor_frames", 9, 5),
+    ("rope_theta", -1.0, 1), ("grid_w", 0, 1),
+])
+def test_invalid_desc_rejected(field, value, status):
+    L = ff.lib()
+    d = desc(**{field: value})
+    assert L.ff_cache_bytes(ctypes.byref(d)) == 0
+    h = ctypes.c_void_p()
+    assert L.ff_cache_create(ctypes.byref(d), FAKE_DEV, 1 << 40, ctypes.byref(h)) == status
+    assert L.ff_last_error()
+
+
+def make_handle(**kw):
+    L = ff.lib()
+    d = desc(**kw)
+    n = L.ff_cache_bytes(ctypes.byref(d))
+    h = ctypes.c_void_p()
+    assert L.ff_cache_create(ctypes.byref(d), FAKE_DEV, n, ctypes.byref(h)) == 0
+    return L, h, n
+
+
+def test_create_checks_buffer():
+    L = ff.lib()
+    d = desc()
+    n = L.ff_cache_bytes(ctypes.byref(d))
+    h = ctypes.c_void_p()
+    assert L.ff_cache_create(ctypes.byref(d), FAKE_DEV, n - 1, ctypes.byref(h)) == 7
+    assert L.ff_cache_create(ctypes.byref(d), FAKE_DEV + 16, n, ctypes.byref(h)) == 7
+    assert L.ff_cache_create(ctypes.byref(d), None, n, ctypes.byref(h)) == 1
+
+
+def test_fresh_cache_state_and_host_validation():
+    L, h, _ = make_handle()
+    slots = (ctypes.c_int64 * 4)()
+    cnt = ctypes.c_int64(-5)
+    assert L.ff_cache_ring_state(h, 3, 1, slots, ctypes.byref(cnt)) == 0
+    assert list(slots) == [-1] * 4 and cnt.value == 0
+    assert L.ff_cache_ring_state(h, 4, 0, slots, ctypes.byref(cnt)) == 4   # stage range
+    assert L.ff_cache_ring_state(h, 0, 2, slots, ctypes.byref(cnt)) == 4   # layer range
+    nfr = ctypes.c_int32(-1)
+    assert L.ff_cache_anchor_state(h, 0, ctypes.byref(nfr), None) == 0 and nfr.value == 0
+    dummy = FAKE_DEV
+    # publish / attention argument checks happen before any launch
+    assert L.ff_kv_publish(h, 9, 0, 0, dummy, dummy, None) == 4
+    assert L.ff_kv_publish(h, 0, 0, -1, dummy, dummy, None) == 4
+    assert L.ff_kv_publish(h, 0, 0, 0, None, dummy, None) == 1
+    assert L.ff_chunk_attention(h, 0, 0, 0, dummy, dummy, dummy, None, 0.1, None) == 1
+    assert L.ff_chunk_attention(h, 0, 0, 0, dummy, dummy, dummy, dummy, 0.0, None) == 1
+    assert L.ff_chunk_attention(h, 0, 0, 0, dummy, dummy, dummy, dummy, float("nan"), None) == 1
+    assert L.ff_chunk_attention(h, 0, 5, 0, dummy, dummy, dummy, dummy, 0.1, None) == 4
+    ft = (ctypes.c_int32 * 4)(0, 10, 20, 30)
+    assert L.ff_anchor_set(h, 0, 4, ft, dummy, dummy, None) == 4        # > max_anchor_frames
+    assert L.ff_anchor_set(h, 0, 2, ft, None, dummy, None) == 1
+    assert L.ff_rope3d(h, dummy, None, 0, ft, None) == 5
+    assert L.ff_rope3d(h, dummy, None, 17, ft, None) == 5
+    neg = (ctypes.c_int32 * 1)(-3)
+    assert L.ff_rope3d(h, dummy, None, 1, neg, None) == 4
+    assert L.ff_cache_read(h, 0, 0, 4, dummy, dummy, None) == 4
+    # misaligned tensors are rejected before any launch
+    assert L.ff_kv_publish(h, 0, 0, 0, dummy + 8, dummy, None) == 1
+    assert L.ff_chunk_attention(h, 0, 0, 0, dummy, dummy, dummy + 2, dummy, 0.1, None) == 1
+    assert L.ff_rope3d(h, dummy + 4, None, 1, ft, None) == 1
+    # anchor_set with 0 frames clears without launching anything
+    assert L.ff_anchor_set(h, 1, 0, None, None, None, None) == 0
+    # state unchanged by the failed calls
+    assert L.ff_cache_ring_state(h, 0, 0, slots, ctypes.byref(cnt)) == 0
+    assert list(slots) == [-1] * 4 and cnt.value == 0
+    assert L.ff_cache_destroy(h) == 0
+    assert L.ff_cache_destroy(None) == 0
+
+
+def test_status_strings():
+    L = ff.lib()
+    for code, name in ff.STATUS_NAMES.items():
+        assert L.ff_status_string(code).decode() == name

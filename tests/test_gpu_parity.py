@@ -1,0 +1,285 @@
+"""GPU parity of the HIP path (through the C ABI) against the float64 oracle.
+
+Bars: cache contents and ring indices bit-exact; RoPE within 1 bf16 ulp of
+the rounded float64 result (float32 tensors: 1e-5); bf16 attention within
+max-abs 2e-2 and relative-L2 5e-3 of float64 per call; float32 attention
+within 1e-5.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import ff_oracle as fo
+from paper_2609_32540_amd import ff
+
+from gpu_util import (PairedRun, bf16_ordered, check_attention, exact, make_cache, make_oracle,
+                      oracle_rope, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _needs_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ff.lib()
+
+
+def small(dtype="bf16", head_dim=128, **kw):
+    base = dict(dtype=dtype, heads=2, head_dim=head_dim, grid_h=6, grid_w=11, ring_chunks=2,
+                stages=2, layers=2, n_chunks=5, anchor_rule="fixed:0,7", max_anchor_frames=3)
+    base.update(kw)
+    return synth.small_workload("small", **base)
+
+
+# --------------------------------------------------------------------------
+# (a3, a4) publish, anchor set: bit-exact contents and indices
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,head_dim", [("bf16", 128), ("bf16", 64), ("f32", 64), ("f32", 128)])
+def test_publish_and_anchor_set_bitexact(dtype, head_dim):
+    w = small(dtype, head_dim, heads=3, grid_h=5, grid_w=7, ring_chunks=3)
+    cache, orc = make_cache(w, 2, 2), make_oracle(w, 2, 2)
+    plan = [(0, 1, c) for c in range(8)] + [(1, 0, c) for c in range(2, 7)]
+    plan = [plan[i] for i in np.random.default_rng(0).permutation(len(plan))]
+    plan.sort(key=lambda t: (t[0], t[1], t[2]))   # per-ring order kept
+    for s, l, c in plan:
+        k = synth.chunk_tensor(w, synth.T_K, c, s, l)
+        v = synth.chunk_tensor(w, synth.T_V, c, s, l)
+        cache.kv_publish(s, l, c, to_dev(k), to_dev(v))
+        orc.publish(s, l, c, exact(k), exact(v))
+        assert cache.ring_state(s, l) == orc.ring_state(s, l)
+    for s in range(2):
+        for l in range(2):
+            table, _ = orc.ring_state(s, l)
+            assert cache.ring_state(s, l)[0] == table
+            entries = {e.chunk: e for e in orc.history.get((s, l), [])}
+            for slot, c in enumerate(table):
+                if c < 0:
+                    continue
+                kg, vg = cache.read(s, l, slot)
+                np.testing.assert_array_equal(exact(kg), entries[c].K)
+                np.testing.assert_array_equal(exact(vg), entries[c].V)
+    # anchors: set, then replace with a different frame count
+    for frames in ([0, 10, 20], [5]):
+        k, v = synth.anchor_tensors(w, frames, 1)
+        cache.anchor_set(1, frames, to_dev(k), to_dev(v))
+        assert cache.anchor_state(1) == frames
+        kg, vg = cache.read(-1, 1)
+        assert torch.equal(kg.cpu(), k) and torch.equal(vg.cpu(), v)
+    assert cache.anchor_state(0) == []
+
+
+def test_ring_wraparound_long_sequence_bitexact():
+    # 87 chunks through a W=4 ring (the long-horizon chunk count)
+    w = small("bf16", 64, heads=1, grid_h=2, grid_w=4, ring_chunks=4)
+    cache, orc = make_cache(w, 1, 1), make_oracle(w, 1, 1)
+    for c in range(87):
+        k = synth.chunk_tensor(w, synth.T_K, c, 0, 0)
+        v = synth.chunk_tensor(w, synth.T_V, c, 0, 0)
+        cache.kv_publish(0, 0, c, to_dev(k), to_dev(v))
+        orc.publish(0, 0, c, exact(k), exact(v))
+        assert cache.ring_state(0, 0) == orc.ring_state(0, 0)
+    Kc, Vc, chunks = orc.history_concat(0, 0)
+    assert chunks == [83, 84, 85, 86]
+    got_k = np.concatenate([exact(cache.read(0, 0, c % 4)[0]) for c in chunks])
+    got_v = np.concatenate([exact(cache.read(0, 0, c % 4)[1]) for c in chunks])
+    np.testing.assert_array_equal(got_k, Kc)
+    np.testing.assert_array_equal(got_v, Vc)
+
+
+def test_order_errors_leave_state_unchanged():
+    w = small("bf16", 128)
+    cache = make_cache(w, 1, 1)
+    k = to_dev(synth.chunk_tensor(w, synth.T_K, 0, 0, 0))
+    cache.kv_publish(0, 0, 3, k, k)
+    before = cache.ring_state(0, 0)
+    with pytest.raises(ff.FFError) as e:
+        cache.kv_publish(0, 0, 5, k, k)
+    assert e.value.status == 3
+    with pytest.raises(ff.FFError) as e:
+        cache.chunk_attention(0, 0, 3, k, k, k)
+    assert e.value.status == 3
+    with pytest.raises(ValueError):
+        cache.kv_publish(0, 0, 4, k[:-1], k[:-1])
+    assert cache.ring_state(0, 0) == before
+    cache.kv_publish(0, 0, 4, k, k)
+    assert cache.ring_state(0, 0) == ([4, 3], 5)
+
+
+# --------------------------------------------------------------------------
+# (a2) RoPE
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,head_dim,grid,heads", [
+    ("bf16", 128, (30, 52), 12), ("bf16", 128, (45, 80), 40), ("bf16", 64, (8, 8), 2),
+    ("f32", 64, (8, 8), 2), ("f32", 128, (6, 11), 3)])
+def test_rope_parity(dtype, head_dim, grid, heads):
+    w = small(dtype, head_dim, heads=heads, grid_h=grid[0], grid_w=grid[1])
+    cache = make_cache(w, 1, 1)
+    frames = [57, 58, 59]
+    q = synth.chunk_tensor(w, synth.T_Q, 19, 0, 0)
+    k = synth.chunk_tensor(w, synth.T_K, 19, 0, 0)
+    qd, kd = to_dev(q), to_dev(k)
+    cache.rope3d(qd, kd, frames)
+    for got, x in ((qd, q), (kd, k)):
+        ref = oracle_rope(w, x, frames)
+        if dtype == "bf16":
+            ref_t = torch.from_numpy(ref.astype(np.float32)).to(torch.bfloat16)
+            d = np.abs(bf16_ordered(got) - bf16_ordered(ref_t))
+            assert d.max() <= 1
+            assert (d > 0).mean() < 1e-3
+        else:
+            assert np.abs(exact(got) - ref).max() <= 1e-5
+    # k only, a single frame at t = 0: frame 0, row 0, col 0 is unrotated
+    k2 = to_dev(synth.chunk_tensor(w, synth.T_K, 0, 0, 0)[: w.tokens_per_frame].contiguous())
+    k2_in = k2.clone()
+    cache.rope3d(None, k2, [0])
+    assert torch.equal(k2[0], k2_in[0])
+
+
+# --------------------------------------------------------------------------
+# (a5) attention
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,head_dim", [("bf16", 128), ("bf16", 64), ("f32", 64), ("f32", 128)])
+def test_attention_direct_inputs(dtype, head_dim):
+    # identical stored inputs on both sides (no RoPE): ragged chunk (198 tokens),
+    # ragged anchors (2 frames = 132 keys), ring wraparound, two stages, two layers
+    w = small(dtype, head_dim)
+    run = PairedRun(w, rope=False)
+    for c in range(w.n_chunks):
+        for s in range(w.stages):
+            for l in range(w.layers):
+                run.step(c, s, l)
+
+
+@pytest.mark.parametrize("dtype,head_dim", [("bf16", 128), ("f32", 64)])
+def test_attention_end_to_end_with_rope(dtype, head_dim):
+    w = small(dtype, head_dim, n_chunks=4)
+    run = PairedRun(w, rope=True)
+    for c in range(w.n_chunks):
+        for s in range(w.stages):
+            for l in range(w.layers):
+                run.step(c, s, l)
+
+
+@pytest.mark.parametrize("layers", [1, 2])
+def test_tiny_workload_end_to_end(layers):
+    # fp32, 2 heads, d 64, 8x8 grid, 3-frame chunks, W=2, 4 stages, anchors at
+    # latent frames 0 and 15, 6 chunks, chunk-major order
+    w = synth.WORKLOADS["tiny-f32"]
+    run = PairedRun(w, layers=layers)
+    for c in range(w.n_chunks):
+        for s in range(w.stages):
+            for l in range(layers):
+                run.step(c, s, l)
+    assert len(run.results) == w.n_chunks * w.stages * layers
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_tiny_shape_bf16(head_dim):
+    w = synth.small_workload("tiny-bf16", dtype="bf16", heads=2, head_dim=head_dim, grid_h=8,
+                             grid_w=8, ring_chunks=2, stages=4, layers=1, n_chunks=6,
+                             anchor_rule="fixed:0,15", max_anchor_frames=2, wid=1)
+    run = PairedRun(w)
+    for c in range(w.n_chunks):
+        for s in range(w.stages):
+            run.step(c, s, 0)
+
+
+def test_attention_degenerate_shapes():
+    # W = 1, no anchor segment, one head, a chunk smaller than one key tile (18 tokens)
+    w = synth.small_workload("deg", dtype="bf16", heads=1, head_dim=128, grid_h=2, grid_w=3,
+                             ring_chunks=1, stages=1, layers=1, n_chunks=4, anchor_rule="none",
+                             max_anchor_frames=1)
+    run = PairedRun(w)
+    for c in range(w.n_chunks):
+        run.step(c, 0, 0)
+
+
+def test_unfilled_slots_poisoned_with_nan_are_never_read():
+    w = small("bf16", 128, ring_chunks=4, anchor_rule="fixed:3", max_anchor_frames=3)
+    run = PairedRun(w, poison=True)
+    for c in range(3):                       # ring never fills; 2 of 3 anchor frames unset
+        for s in range(w.stages):
+            for l in range(w.layers):
+                run.step(c, s, l)
+
+
+def test_softmax_scale_argument():
+    w = small("bf16", 128, n_chunks=2)
+    run = PairedRun(w)
+    for c in range(2):
+        run.step(c, 0, 0, scale=0.3)
+
+
+def test_deterministic_and_order_independent():
+    # chunk-major order and the anti-diagonal wavefront order of the paper's
+    # batched rollout (round n runs chunk n - r at stage r) give the same bits
+    w = small("bf16", 128, stages=4, layers=1, n_chunks=5)
+    outs = {}
+    for order_name in ("chunk-major", "wavefront", "chunk-major-again"):
+        cache = make_cache(w, 4, 1)
+        k, v = synth.anchor_tensors(w, [0, 7], 0)
+        cache.anchor_set(0, [0, 7], to_dev(k), to_dev(v))
+        if order_name == "wavefront":
+            order = [(n - r, r) for n in range(w.n_chunks + 3) for r in range(4)
+                     if 0 <= n - r < w.n_chunks]
+        else:
+            order = [(c, s) for c in range(w.n_chunks) for s in range(4)]
+        res = {}
+        for c, s in order:
+            q = to_dev(synth.chunk_tensor(w, synth.T_Q, c, s, 0))
+            kk = to_dev(synth.chunk_tensor(w, synth.T_K, c, s, 0))
+            vv = to_dev(synth.chunk_tensor(w, synth.T_V, c, s, 0))
+            res[(c, s)] = cache.chunk_attention(s, 0, c, q, kk, vv).cpu()
+            cache.kv_publish(s, 0, c, kk, vv)
+        outs[order_name] = res
+    for key in outs["chunk-major"]:
+        assert torch.equal(outs["chunk-major"][key], outs["wavefront"][key]), key
+        assert torch.equal(outs["chunk-major"][key], outs["chunk-major-again"][key]), key
+
+
+# --------------------------------------------------------------------------
+# long horizon: 87 chunks, anchor updates every 8 chunks, ring wraparound
+# --------------------------------------------------------------------------
+
+def test_long_horizon_schedule():
+    base = synth.WORKLOADS["1.3b-480p-long"]
+    # same chunk count, anchor schedule, W, head_dim and input scale; reduced grid and heads
+    w = synth.small_workload("long-reduced", dtype="bf16", heads=2, head_dim=128, grid_h=4,
+                             grid_w=7, ring_chunks=base.ring_chunks, stages=1, layers=1,
+                             n_chunks=base.n_chunks, input_scale=base.input_scale,
+                             anchor_rule=base.anchor_rule, max_anchor_frames=3, wid=base.wid)
+    run = PairedRun(w)
+    for c in range(w.n_chunks):
+        run.step(c, 0, 0)
+    assert run.cache.anchor_state(0) == [0, 240, 260]
+    assert run.cache.ring_state(0, 0) == ([84, 85, 86, 83], 87)
+
+
+# --------------------------------------------------------------------------
+# full-size workloads: one steady-state chunk-stage, sampled rows
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["1.3b-480p", "14b-480p", "14b-720p"])
+def test_full_size_sampled_rows(name):
+    w = synth.WORKLOADS[name]
+    stage, layer, chunk = 1, 3, w.ring_chunks + 3          # ring full, steady state
+    run = PairedRun(w, stages=stage + 1, layers=layer + 1, rope=False)
+    nq = w.chunk_tokens
+    rows = np.concatenate([np.arange(0, 512), np.arange(nq - 512, nq)])   # includes the ragged tail tile
+    heads = [0, w.heads - 1]
+    for c in range(chunk - w.ring_chunks, chunk + 1):
+        run.step(c, stage, layer, check=(c == chunk), rows=rows, heads=heads)
+    # the ring holds the previous W chunks plus this one; check one full slot bit for bit
+    table, count = run.cache.ring_state(stage, layer)
+    assert count == chunk + 1 and sorted(table) == list(range(chunk - w.ring_chunks + 1, chunk + 1))
+    entries = {e.chunk: e for e in run.oracle.history[(stage, layer)]}
+    kg, vg = run.cache.read(stage, layer, chunk % w.ring_chunks)
+    np.testing.assert_array_equal(exact(kg), entries[chunk].K)
+    np.testing.assert_array_equal(exact(vg), entries[chunk].V)

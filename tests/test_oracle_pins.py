@@ -288,13 +288,19 @@ def test_read_set_window_and_anchor_replacement():
     cache.anchor_set(0, [10, 20], a2, a2)     # replaces, does not append
     for c in range(3):
         cache.publish(0, 0, c, np.full((3, 1, 2), c), np.full((3, 1, 2), c))
-    K, V, vis = cache.read_set(0, 0, 3, np.full((3, 1, 2), 9.0), np.full((3, 1, 2), 9.0))
-    assert K.shape[0] == 8 + 2 * 3 + 3
-    np.testing.assert_array_equal(K[:8], a2)
+    Ks, Vs, vis = cache.read_set(0, 0, 3, np.full((3, 1, 2), 9.0), np.full((3, 1, 2), 9.0))
+    assert [k.shape[0] for k in Ks] == [8, 3, 3, 3]
+    np.testing.assert_array_equal(Ks[0], a2)
     # history holds chunks 1 and 2; both are in [3-W, 2]
-    np.testing.assert_array_equal(K[8:11, 0, 0], [1, 1, 1])
-    np.testing.assert_array_equal(K[11:14, 0, 0], [2, 2, 2])
-    assert vis.all()
+    np.testing.assert_array_equal(Ks[1][:, 0, 0], [1, 1, 1])
+    np.testing.assert_array_equal(Ks[2][:, 0, 0], [2, 2, 2])
+    assert vis == [True, True, True, True]
+    # seen from chunk 4 (history not advanced), chunk 1 falls out of [4-W, 3]
+    cache2 = fo.RendererCacheOracle(stages=1, layers=1, W=W)
+    for c in range(3):
+        cache2.publish(0, 0, c, np.full((3, 1, 2), c), np.full((3, 1, 2), c))
+    _, _, vis = cache2.read_set(0, 0, 4, np.zeros((3, 1, 2)), np.zeros((3, 1, 2)))
+    assert vis == [False, True, True]
 
 
 def _stage_sequence(seed, n_chunks, W, nq, h, d, anchors_of_chunk, anchor_data):
