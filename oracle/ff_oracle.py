@@ -152,18 +152,24 @@ def rope3d(X: np.ndarray, frame_t: Sequence[int], grid_h: int, grid_w: int,
 # (a5) attention over an explicit visibility mask
 # --------------------------------------------------------------------------
 
+def attend(Qh: np.ndarray, Kh: np.ndarray, Vh: np.ndarray, scale: float) -> np.ndarray:
+    """softmax(scale * Qh Kh^T) Vh for one head, in float64: Qh [nq, d], Kh, Vh [nk, d]."""
+    s = scale * (np.asarray(Qh, np.float64) @ np.asarray(Kh, np.float64).T)   # [nq, nk]
+    m = s.max(axis=1, keepdims=True)
+    p = np.exp(s - m)
+    return (p @ np.asarray(Vh, np.float64)) / p.sum(axis=1, keepdims=True)
+
+
 def masked_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, visible: np.ndarray,
                      scale: float, heads: Optional[Sequence[int]] = None,
                      rows: Optional[np.ndarray] = None) -> np.ndarray:
     """softmax(scale * Q K^T) V per head over the visible keys only.
 
-    Q [nq, h, d]; K, V [nk, h, d]; visible: bool [nk].  Returns float64
+    Q [nq, h, d]; K, V [nk, h, d]; visible: bool [nk].  Keys that are not
+    visible are dropped before any arithmetic.  Returns float64
     [len(rows), len(heads), d] (all rows / heads when not given).
     """
     visible = np.asarray(visible, dtype=bool)
-    Kv = np.asarray(K, dtype=np.float64)[visible]
-    Vv = np.asarray(V, dtype=np.float64)[visible]
-    Q = np.asarray(Q, dtype=np.float64)
     if heads is None:
         heads = range(Q.shape[1])
     if rows is None:
@@ -171,10 +177,7 @@ def masked_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, visible: np.nd
     heads = list(heads)
     out = np.empty((len(rows), len(heads), Q.shape[2]), dtype=np.float64)
     for hi, h in enumerate(heads):
-        s = scale * (Q[rows, h, :] @ Kv[:, h, :].T)           # [rows, n_visible]
-        m = s.max(axis=1, keepdims=True)
-        p = np.exp(s - m)
-        out[:, hi, :] = (p @ Vv[:, h, :]) / p.sum(axis=1, keepdims=True)
+        out[:, hi, :] = attend(Q[rows, h, :], K[visible, h, :], V[visible, h, :], scale)
     return out
 
 
@@ -212,8 +215,7 @@ class RendererCacheOracle:
         """Replace layer ``layer``'s anchor segment (already-rotated K, and V)."""
         if not 0 <= layer < self.layers:
             raise IndexError(layer)
-        self.anchors[layer] = (list(frames), np.array(K, dtype=np.float64),
-                               np.array(V, dtype=np.float64))
+        self.anchors[layer] = (list(frames), np.array(K), np.array(V))
 
     def publish(self, stage: int, layer: int, i: int, K: np.ndarray, V: np.ndarray) -> None:
         """Eq. step-update: B <- Tail_W(B u (i, K, V)); chunks arrive in order."""
@@ -222,7 +224,7 @@ class RendererCacheOracle:
         if expected is not None and i != expected:
             raise OrderError(f"publish chunk {i}, expected {expected}")
         lst = self.history.setdefault(key, [])
-        lst.append(HistoryEntry(i, np.array(K, dtype=np.float64), np.array(V, dtype=np.float64)))
+        lst.append(HistoryEntry(i, np.array(K), np.array(V)))
         while len(lst) > self.W:
             lst.pop(0)
         self.next_chunk[key] = i + 1
@@ -244,8 +246,8 @@ class RendererCacheOracle:
                 [e.chunk for e in lst])
 
     def read_set(self, stage: int, layer: int, i: int, K_cur: np.ndarray, V_cur: np.ndarray
-                 ) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
-        """Full key list [anchors | history entries | current] and its visibility.
+                 ) -> Tuple[List[np.ndarray], List[np.ndarray], List[bool]]:
+        """Key segments [anchors | history entries | current] and their visibility.
 
         Anchors: every frame of the layer's anchor segment.  History: entries
         whose chunk lies in [max(0, i-W), i-1] (same stage).  Current chunk:
@@ -255,14 +257,12 @@ class RendererCacheOracle:
         Ks, Vs, vis = [], [], []
         if layer in self.anchors:
             _, Ka, Va = self.anchors[layer]
-            Ks.append(Ka); Vs.append(Va); vis.append(np.ones(Ka.shape[0], bool))
+            Ks.append(Ka); Vs.append(Va); vis.append(True)
         for e in self.history.get(key, []):
             Ks.append(e.K); Vs.append(e.V)
-            vis.append(np.full(e.K.shape[0], max(0, i - self.W) <= e.chunk <= i - 1))
-        Kc = np.asarray(K_cur, dtype=np.float64)
-        Vc = np.asarray(V_cur, dtype=np.float64)
-        Ks.append(Kc); Vs.append(Vc); vis.append(np.ones(Kc.shape[0], bool))
-        return np.concatenate(Ks, 0), np.concatenate(Vs, 0), np.concatenate(vis, 0)
+            vis.append(max(0, i - self.W) <= e.chunk <= i - 1)
+        Ks.append(np.asarray(K_cur)); Vs.append(np.asarray(V_cur)); vis.append(True)
+        return Ks, Vs, vis
 
     def attention(self, stage: int, layer: int, i: int, Q: np.ndarray, K_cur: np.ndarray,
                   V_cur: np.ndarray, scale: Optional[float] = None,
@@ -275,8 +275,18 @@ class RendererCacheOracle:
             raise OrderError(f"attention for chunk {i}, history expects {expected}")
         if scale is None:
             scale = 1.0 / math.sqrt(Q.shape[2])
-        K, V, vis = self.read_set(stage, layer, i, K_cur, V_cur)
-        return masked_attention(Q, K, V, vis, scale, heads=heads, rows=rows)
+        Ks, Vs, vis = self.read_set(stage, layer, i, K_cur, V_cur)
+        if heads is None:
+            heads = range(Q.shape[1])
+        if rows is None:
+            rows = np.arange(Q.shape[0])
+        heads = list(heads)
+        out = np.empty((len(rows), len(heads), Q.shape[2]), dtype=np.float64)
+        for hi, h in enumerate(heads):
+            Kh = np.concatenate([k[:, h, :] for k, v_ in zip(Ks, vis) if v_], 0)
+            Vh = np.concatenate([v[:, h, :] for v, v_ in zip(Vs, vis) if v_], 0)
+            out[:, hi, :] = attend(Q[rows, h, :], Kh, Vh, scale)
+        return out
 
 
 # --------------------------------------------------------------------------
