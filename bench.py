@@ -1,0 +1,269 @@
+"""Benchmark of the FlashForward renderer-attention hot path on one MI355X.
+
+One step = one chunk-stage forward of the renderer over every layer of the
+workload: for each layer, 3D RoPE of the chunk's Q/K, attention of the chunk
+over [anchor segment | stage-matched history ring | the chunk itself], and
+publish of the chunk's K/V into the ring (plus the anchor-segment update when
+the chunk enters a new anchor window).  Steps walk chunk-major through the
+stages (chunk i at stages 0..S-1, then chunk i+1), starting with every ring
+full, so each step is a steady-state chunk-stage.  Inputs are synthetic
+(seeded N(0,1) on the device), one buffer set per layer so the 256 MB
+Infinity Cache does not hold the previous layer's data.
+
+Prints one JSON line.  `value` is attention TFLOP/s over the whole timed
+region (attention FLOPs of every step / wall time of the steps, RoPE and
+publish included); the per-kernel breakdown, the roofline of the attention
+kernel and the CPU oracle baseline are attached.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+from paper_2609_32540_amd import ff  # noqa: E402
+
+METRIC = "attention TFLOP/s + ms per chunk-stage forward (attn+publish), % bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak (published)
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E (published)
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class Workspace:
+    """Cache, per-layer input buffers and the step schedule of one workload."""
+
+    def __init__(self, w: synth.Workload, seed: int = 0):
+        self.w = w
+        dev = torch.device("cuda", 0)
+        self.dev = dev
+        self.cache = ff.RendererCache(stages=w.stages, layers=w.layers, ring_chunks=w.ring_chunks,
+                                      frames_per_chunk=w.frames_per_chunk, grid_h=w.grid_h,
+                                      grid_w=w.grid_w, heads=w.heads, head_dim=w.head_dim,
+                                      max_anchor_frames=w.max_anchor_frames, dtype=w.torch_dtype,
+                                      device=dev)
+        g = torch.Generator(device=dev)
+        g.manual_seed(seed)
+        shape = (w.chunk_tokens, w.heads, w.head_dim)
+
+        def randn(s):
+            return (torch.randn(s, generator=g, device=dev, dtype=torch.float32)
+                    * w.input_scale).to(w.torch_dtype)
+
+        self.q = [randn(shape) for _ in range(w.layers)]
+        self.k = [randn(shape) for _ in range(w.layers)]
+        self.v = [randn(shape) for _ in range(w.layers)]
+        self.out = [torch.empty(shape, dtype=w.torch_dtype, device=dev) for _ in range(w.layers)]
+        a_shape = (w.max_anchor_frames * w.tokens_per_frame, w.heads, w.head_dim)
+        self.anchor_k = [randn(a_shape) for _ in range(w.layers)]
+        self.anchor_v = [randn(a_shape) for _ in range(w.layers)]
+        self.anchor_frames = None
+        # fill every ring with W chunks (chunks 0 .. W-1) so the steps run at steady state
+        for s in range(w.stages):
+            for l in range(w.layers):
+                for c in range(w.ring_chunks):
+                    self.cache.kv_publish(s, l, c, self.k[l], self.v[l])
+        self.next = (w.ring_chunks, 0)  # (chunk, stage) of the next step
+        torch.cuda.synchronize()
+
+    def kv_tokens(self, chunk: int) -> int:
+        w = self.w
+        n_hist = min(chunk, w.ring_chunks)
+        return (len(w.anchor_frames_for_chunk(chunk)) * w.tokens_per_frame
+                + n_hist * w.chunk_tokens + w.chunk_tokens)
+
+    def attn_flops(self, chunk: int) -> float:
+        w = self.w
+        return 4.0 * w.chunk_tokens * self.kv_tokens(chunk) * w.head_dim * w.heads
+
+    def step(self, events=None) -> float:
+        """Enqueue one chunk-stage forward; returns its attention FLOPs (all layers)."""
+        w = self.w
+        chunk, stage = self.next
+        frames_a = w.anchor_frames_for_chunk(chunk)
+        n_a = len(frames_a) * w.tokens_per_frame
+        new_window = frames_a != self.anchor_frames
+        frames = [chunk * w.frames_per_chunk + f for f in range(w.frames_per_chunk)]
+        for l in range(w.layers):
+            if new_window:
+                ak = self.anchor_k[l][:n_a]
+                self.cache.rope3d(None, ak, frames_a)
+                self.cache.anchor_set(l, frames_a, ak, self.anchor_v[l][:n_a])
+            if events is not None:
+                events[l][0].record()
+            self.cache.rope3d(self.q[l], self.k[l], frames)
+            if events is not None:
+                events[l][1].record()
+            self.cache.chunk_attention(stage, l, chunk, self.q[l], self.k[l], self.v[l], self.out[l])
+            if events is not None:
+                events[l][2].record()
+            self.cache.kv_publish(stage, l, chunk, self.k[l], self.v[l])
+            if events is not None:
+                events[l][3].record()
+        self.anchor_frames = frames_a
+        self.next = (chunk, stage + 1) if stage + 1 < w.stages else (chunk + 1, 0)
+        return self.attn_flops(chunk) * w.layers
+
+
+def cpu_baseline(w: synth.Workload, target_s: float = 12.0) -> dict:
+    """The float64 oracle's attention on 1-head x 512-query slices at the full key length."""
+    from oracle import ff_oracle as fo
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    chunk = w.ring_chunks + 1
+    nkv = (len(w.anchor_frames_for_chunk(chunk)) * w.tokens_per_frame
+           + w.ring_chunks * w.chunk_tokens + w.chunk_tokens)
+    rows = 512
+    d = w.head_dim
+    Q = synth.normal_rows([0, w.wid, 1000, 0, 0, synth.T_Q], rows, d, w.input_scale, w.torch_dtype)
+    K = synth.normal_rows([0, w.wid, 1000, 0, 0, synth.T_K], nkv, d, w.input_scale, w.torch_dtype)
+    V = synth.normal_rows([0, w.wid, 1000, 0, 0, synth.T_V], nkv, d, w.input_scale, w.torch_dtype)
+    Qn, Kn, Vn = (t.float().numpy() for t in (Q, K, V))
+    scale = 1.0 / math.sqrt(d)
+    fo.attend(Qn[:8], Kn, Vn, scale)   # warm the BLAS threads
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        fo.attend(Qn, Kn, Vn, scale)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= target_s or n >= 200:
+            break
+    flops = 4.0 * rows * nkv * d * n
+    return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} x (1 head x {rows} queries x {nkv} keys x d {d}) of the float64 oracle "
+                      f"attention, {el:.1f} s; full chunk-stage = {w.heads * w.layers} heads x "
+                      f"{w.chunk_tokens} queries",
+            "seconds": round(el, 2)}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=8)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="14b-720p", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--breakdown-steps", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the stage-per-GPU "
+              "split of the paper is not part of this build", file=sys.stderr)
+        return 2
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    w = synth.WORKLOADS[args.workload]
+    if w.dtype != "bf16":
+        print("the benchmark workloads are the bf16 ones", file=sys.stderr)
+        return 2
+    ff.lib()
+    log(f"workload {w.name}: {w.heads} heads x {w.head_dim}, {w.chunk_tokens} queries, "
+        f"{w.layers} layers, {w.stages} stages")
+    t0 = time.time()
+    ws = Workspace(w)
+    log(f"allocated {ws.cache.nbytes / 2**30:.1f} GiB cache, rings filled ({time.time() - t0:.1f} s)")
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        ws.step()
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    # timed region: K steps bracketed by events on the launch stream
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    flops = 0.0
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        flops += ws.step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    ms_per_step = ms_total / args.steps
+    value = flops / (ms_total * 1e-3) / 1e12
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {value:.1f} TFLOP/s")
+
+    # per-kernel breakdown: events between the launches of each layer
+    bd_steps = max(1, args.breakdown_steps)
+    rope_ms, attn_ms, pub_ms, attn_flops = [], [], [], []
+    for _ in range(bd_steps):
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(w.layers)]
+        chunk = ws.next[0]
+        ws.step(ev)
+        torch.cuda.synchronize()
+        for l in range(w.layers):
+            rope_ms.append(ev[l][0].elapsed_time(ev[l][1]))
+            attn_ms.append(ev[l][1].elapsed_time(ev[l][2]))
+            pub_ms.append(ev[l][2].elapsed_time(ev[l][3]))
+            attn_flops.append(ws.attn_flops(chunk))
+    attn_avg = float(np.mean(attn_ms))
+    pub_avg = float(np.mean(pub_ms))
+    rope_avg = float(np.mean(rope_ms))
+    attn_achieved = float(np.mean(attn_flops)) / (attn_avg * 1e-3) / 1e12
+    elem = 2
+    pub_bytes = 4.0 * w.chunk_tokens * w.heads * w.head_dim * elem
+    rope_bytes = 4.0 * w.chunk_tokens * w.heads * w.head_dim * elem
+    pub_gbs = pub_bytes / (pub_avg * 1e-3) / 1e9
+    rope_gbs = rope_bytes / (rope_avg * 1e-3) / 1e9
+    log(f"attention {attn_avg:.3f} ms/launch = {attn_achieved:.1f} TFLOP/s; publish {pub_avg*1e3:.1f} us "
+        f"= {pub_gbs:.0f} GB/s; rope {rope_avg*1e3:.1f} us = {rope_gbs:.0f} GB/s")
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "heads": w.heads, "head_dim": w.head_dim,
+                   "grid": f"{w.grid_h}x{w.grid_w}", "chunk_tokens": w.chunk_tokens,
+                   "kv_tokens": ws.kv_tokens(w.ring_chunks + 1), "ring_chunks": w.ring_chunks,
+                   "stages": w.stages, "layers": w.layers, "anchor_frames": 3},
+        "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "ms_attn_publish_per_chunk_stage": round((attn_avg + pub_avg) * w.layers, 3),
+        "ms_rope_per_chunk_stage": round(rope_avg * w.layers, 3),
+        "kernels": {
+            "attention": {"ms_per_launch": round(attn_avg, 4), "tflops": round(attn_achieved, 2),
+                          "pct_bf16_peak": round(100 * attn_achieved / PEAK_BF16_TFLOPS, 2)},
+            "kv_publish": {"us_per_launch": round(pub_avg * 1e3, 2), "gbs": round(pub_gbs, 1),
+                           "pct_hbm_peak": round(100 * pub_gbs / PEAK_HBM_GBS, 2)},
+            "rope3d": {"us_per_launch": round(rope_avg * 1e3, 2), "gbs": round(rope_gbs, 1),
+                       "pct_hbm_peak": round(100 * rope_gbs / PEAK_HBM_GBS, 2)},
+        },
+        "roofline": {"bound": "mfma", "achieved": round(attn_achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle")
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -130,8 +130,9 @@ ff_status ff_cache_destroy(ff_cache* cache);
  * [n_t, n_t + n_h) use the row and the rest the column, and j counts pairs
  * inside the axis block: (a, b) -> (a cos phi - b sin phi, a sin phi + b cos phi).
  * The paper fixes no RoPE; this is the convention of its Wan2.1 backbone.
- * Rotation runs in float32 with angles from float64; bf16 results are
- * rounded to nearest even.  1 <= n_frames <= FF_MAX_ROPE_FRAMES. */
+ * Angles, cosines, sines and the rotation are evaluated in float64 and
+ * rounded once to the storage type (nearest even).
+ * 1 <= n_frames <= FF_MAX_ROPE_FRAMES. */
 ff_status ff_rope3d(const ff_cache* cache, void* q, void* k, int32_t n_frames,
                     const int32_t* frame_t, void* stream);
 

@@ -4,9 +4,10 @@
 // with pos the token's latent time t for p < n_t, its grid row for
 // n_t <= p < n_th and its grid column otherwise (omega[p] is theta^(-j/n_axis),
 // computed on the host in float64).  The angle and its cosine and sine are
-// computed once per (token, pair) in float64, rounded to float32, kept in LDS
-// and reused by every head of Q and K; the rotation itself runs in float32
-// (bf16 tensors) or float64 (float32 tensors), rounded to nearest even.
+// computed once per (token, pair) in float64, kept in LDS and reused by every
+// head of Q and K.  The rotation runs in float64 and is rounded once to the
+// storage type, to nearest even: for bf16 through a round-to-odd float32
+// intermediate, which makes the two-step rounding equal to a direct one.
 //
 // Launch shape: one block of 256 threads per kTok tokens.  The block's tokens
 // form one contiguous run of kTok * heads * d elements in each tensor, swept
@@ -34,11 +35,23 @@ __device__ inline uint32_t pack_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, h);
 }
 
-__device__ inline uint32_t rotate_bf16_pair(uint32_t w, float2 cs) {
-  const float a = bf16_lo(w), b = bf16_hi(w);
-  const float o0 = fmaf(a, cs.x, -b * cs.y);
-  const float o1 = fmaf(a, cs.y, b * cs.x);
-  return pack_bf16(o0, o1);
+// float64 -> float32 rounded to odd: truncate toward zero and set the last
+// bit when inexact.  Rounding that result to bf16 (8 significant bits, far
+// fewer than float32's 24) to nearest even equals rounding x directly.
+__device__ inline float round_to_odd_f32(double x) {
+  const float r = float(x);  // nearest even
+  const double rd = double(r);
+  if (rd == x) return r;
+  uint32_t bits = __float_as_uint(r);
+  if (fabs(rd) > fabs(x)) bits -= 1;  // one step toward zero
+  return __uint_as_float(bits | 1u);
+}
+
+__device__ inline uint32_t rotate_bf16_pair(uint32_t w, double2 cs) {
+  const double a = bf16_lo(w), b = bf16_hi(w);
+  const double o0 = a * cs.x - b * cs.y;
+  const double o1 = a * cs.y + b * cs.x;
+  return pack_bf16(round_to_odd_f32(o0), round_to_odd_f32(o1));
 }
 
 template <typename T, int D>
@@ -46,8 +59,7 @@ __global__ __launch_bounds__(kThreads) void rope3d_kernel(T* __restrict__ q, T* 
                                                           int n_tok, int heads, int grid_w,
                                                           int tokens_per_frame, RopeParams p) {
   constexpr int P = D / 2;
-  __shared__ float2 cs_f[kTok][P];
-  __shared__ double2 cs_d[(sizeof(T) == 4) ? kTok : 1][P];
+  __shared__ double2 cs_d[kTok][P];
   const int tok0 = blockIdx.x * kTok;
 
   for (int e = threadIdx.x; e < kTok * P; e += kThreads) {
@@ -61,8 +73,7 @@ __global__ __launch_bounds__(kThreads) void rope3d_kernel(T* __restrict__ q, T* 
       const int pos = pr < p.n_t ? p.frame_t[f] : (pr < p.n_th ? y : x);
       double s, c;
       sincos(double(pos) * p.omega[pr], &s, &c);
-      cs_f[tt][pr] = make_float2(float(c), float(s));
-      if constexpr (sizeof(T) == 4) cs_d[tt][pr] = make_double2(c, s);
+      cs_d[tt][pr] = make_double2(c, s);
     }
   }
   __syncthreads();
@@ -82,10 +93,10 @@ __global__ __launch_bounds__(kThreads) void rope3d_kernel(T* __restrict__ q, T* 
       uint4 w = v[e];
       if constexpr (sizeof(T) == 2) {
         const int p0 = c * 4;              // 4 pairs per vector
-        w.x = rotate_bf16_pair(w.x, cs_f[tt][p0 + 0]);
-        w.y = rotate_bf16_pair(w.y, cs_f[tt][p0 + 1]);
-        w.z = rotate_bf16_pair(w.z, cs_f[tt][p0 + 2]);
-        w.w = rotate_bf16_pair(w.w, cs_f[tt][p0 + 3]);
+        w.x = rotate_bf16_pair(w.x, cs_d[tt][p0 + 0]);
+        w.y = rotate_bf16_pair(w.y, cs_d[tt][p0 + 1]);
+        w.z = rotate_bf16_pair(w.z, cs_d[tt][p0 + 2]);
+        w.w = rotate_bf16_pair(w.w, cs_d[tt][p0 + 3]);
       } else {
         const int p0 = c * 2;              // 2 pairs per vector
         const double2 c0 = cs_d[tt][p0], c1 = cs_d[tt][p0 + 1];

@@ -1,7 +1,8 @@
 """GPU parity of the HIP path (through the C ABI) against the float64 oracle.
 
 Bars: cache contents and ring indices bit-exact; RoPE within 1 bf16 ulp of
-the rounded float64 result (float32 tensors: 1e-5); bf16 attention within
+the rounded float64 result, differing only where the two float64 evaluations
+straddle a rounding tie (float32 tensors: 1e-5); bf16 attention within
 max-abs 2e-2 and relative-L2 5e-3 of float64 per call; float32 attention
 within 1e-5.
 """
@@ -131,7 +132,7 @@ def test_rope_parity(dtype, head_dim, grid, heads):
             ref_t = torch.from_numpy(ref.astype(np.float32)).to(torch.bfloat16)
             d = np.abs(bf16_ordered(got) - bf16_ordered(ref_t))
             assert d.max() <= 1
-            assert (d > 0).mean() < 1e-3
+            assert (d > 0).mean() < 1e-5
         else:
             assert np.abs(exact(got) - ref).max() <= 1e-5
     # k only, a single frame at t = 0: frame 0, row 0, col 0 is unrotated
