@@ -1,26 +1,32 @@
 // bf16 renderer attention on gfx950 matrix cores (flash-attention forward).
 //
-// One workgroup = 4 waves = 256 queries of one head; each wave owns 64
-// queries (two 32-query column blocks) for the whole key loop.  Keys arrive as
-// segments (anchor segment, history slots, current chunk); each segment is cut
-// into 64-key tiles, and only a segment's last tile is partial (its missing
-// keys are masked to -inf), so no tile straddles two segments.
+// Work split: a workgroup = 4 waves = 128 queries of one head; each wave owns
+// 32 queries for the whole key loop; two workgroups share a CU, so one's
+// softmax overlaps the other's matrix ops.  Keys arrive as segments (anchor
+// segment, valid history slots, current chunk); each segment is cut into
+// 64-key tiles and only a segment's last tile is partial (its missing keys
+// are masked to -inf): no tile straddles two segments and no empty slot is
+// touched.
 //
 // Per tile:
-//   S^T = K Q^T     v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = Q^T held
-//                   in registers for the whole loop (loaded once).
-//   softmax         S^T's accumulator layout puts one query column in each
-//                   lane (32 of its keys per 32-key block, the other 32 in lane
-//                   ^ 32), so the running max / sum are in-lane except for one
-//                   cross-half exchange of the max; exp2 with log2(e) folded
-//                   into the scale.
-//   O^T += V^T P^T  A = V^T from LDS, B = P^T = the softmax registers rounded
-//                   to bf16 (nearest even) without leaving the lane; the order
-//                   of keys inside each 16-key group of the V^T tile is permuted
-//                   at staging time to match the accumulator layout.
-// K and V tiles are loaded from HBM with 16-byte loads one tile ahead (into
-// registers), then staged in LDS: K row-major with a 16-byte row pad, V
-// transposed with an XOR swizzle of 16-byte chunks.
+//   S^T = K Q^T     v_mfma_f32_32x32x16_bf16; A = K rows read from LDS, B = the
+//                   wave's Q^T, held in registers for the whole loop.
+//   softmax         the accumulator layout of S^T puts one query column in each
+//                   lane (half of the tile's keys; the other half is in lane ^ 32),
+//                   so max and sum are in-lane plus one v_permlane32_swap.  exp2
+//                   with log2(e) folded into the scale.  The running max is only
+//                   raised (and O rescaled) when a column max exceeds it by more
+//                   than 2^8; otherwise the stale max is kept, which leaves the
+//                   result exact since the final sum uses the same max.
+//   O^T += V^T P^T  A = V^T, read from the row-major V tile with the gfx950
+//                   transposing LDS read (ds_read_b64_tr_b16); B = P^T, the
+//                   softmax registers rounded to bf16 in place.  The keys of each
+//                   8-key operand are chosen to match the accumulator layout.
+// K and V tiles are copied from HBM straight into LDS (global_load_lds_dwordx4,
+// 16 bytes per lane) one tile ahead, into a double buffer: one barrier per
+// tile.  Tile rows are stored without padding, with an XOR swizzle of their
+// 16-byte chunks that keeps both the K reads and the transposing V reads free
+// of bank conflicts.
 // Workgroups are renumbered so that consecutive Q tiles of one head land on
 // the same XCD (the hardware deals workgroups to the 8 XCDs round robin) and
 // share that XCD's L2 for the head's K/V.
@@ -38,49 +44,61 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+#define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
+#define GLOBAL_PTR(p) ((const __attribute__((address_space(1))) void*)(p))
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kQB = 2;                      // 32-query column blocks per wave
-constexpr int kWaveQ = 32 * kQB;            // queries per wave
+constexpr int kWaveQ = 32;                  // queries per wave
 constexpr int kBlockQ = kWaves * kWaveQ;    // queries per workgroup
 constexpr int kBK = 64;                     // keys per tile
 constexpr int kXcds = 8;
+constexpr float kRescaleThreshold = 8.0f;   // log2 units
 
 template <int D>
 struct Cfg {
-  static constexpr int KS = D / 16;                 // 16-wide slices of d in S^T = K Q^T
-  static constexpr int DB = D / 32;                 // 32-row blocks of O^T
-  static constexpr int CPR = D / 8;                 // 16-byte chunks per K/V row
-  static constexpr int KPT = kBK * CPR / kThreads;  // consecutive keys staged per thread
-  static constexpr int K_ROW = D * 2 + 16;          // LDS bytes per K row
-  static constexpr int V_ROW = kBK * 2;             // LDS bytes per V^T row
-  static constexpr int LDS_K = kBK * K_ROW;
-  static constexpr int LDS_V = D * V_ROW;
+  static constexpr int KS = D / 16;          // 16-wide d slices of S^T = K Q^T
+  static constexpr int DB = D / 32;          // 32-row blocks of O^T
+  static constexpr int ROWB = 2 * D;         // bytes per K/V row in LDS
+  static constexpr int CPR = D / 8;          // 16-byte chunks per row
+  static constexpr int RPB = 1024 / ROWB;    // rows per 1 KB wave copy
+  static constexpr int BLOCKS = kBK / RPB;   // 1 KB copies per tile (per tensor)
+  static constexpr int BLOCKS_PER_WAVE = BLOCKS / kWaves;
+  static constexpr int TILE = kBK * ROWB;    // bytes of one K (or V) tile
+  static constexpr int BUF = 2 * TILE;       // K tile then V tile
 };
+
+// XOR swizzle of the 16-byte chunks of tile row r: over any 8 consecutive rows
+// it is a permutation of 0..7 (K reads: 32 rows, one chunk), and over any 4
+// rows starting at a multiple of 4 its halves are distinct (V transposing
+// reads: 4 rows x 2 adjacent chunks).
+__device__ inline int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
 
 __device__ inline uint32_t pack_bf16(float a, float b) {
   f32x2 f = {a, b};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
 }
 
-// Position of key o (0..63) inside a V^T row: bits 2 and 3 of the offset in its
-// 16-key group are swapped, so that the 8 keys one lane feeds to a PV matrix
-// op are contiguous.
-__device__ inline int vt_pos(int o) { return (o & ~12) | ((o & 4) << 1) | ((o & 8) >> 1); }
+__device__ inline float max_across_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
 
-// XOR swizzle of the 16-byte chunks of V^T row d.
-__device__ inline int vt_swz(int d) { return (d ^ (d >> 3)) & 7; }
+__device__ inline float sum_across_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, int nq, int heads,
                       float scale_log2, KvSegments segs, int n_qtiles) {
   using C = Cfg<D>;
-  __shared__ __attribute__((aligned(16))) char lds_k[C::LDS_K];
-  __shared__ __attribute__((aligned(16))) char lds_v[C::LDS_V];
+  __shared__ __attribute__((aligned(1024))) char lds[2 * C::BUF];
 
   // XCD-aware renumbering: hardware block b runs on XCD b % 8; give each XCD a
   // contiguous range of logical tiles.
@@ -98,83 +116,57 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   const int l32 = lane & 31;
   const int half = lane >> 5;
 
-  // Q^T operand: lane (l32, half) of column block cb holds query
-  // q0 + cb*32 + l32, elements d = 16 s + 8 half .. +7 for slice s.
-  const int q_wave0 = qt * kBlockQ + wave * kWaveQ;
-  bf16x8 qreg[kQB][C::KS];
-#pragma unroll
-  for (int cb = 0; cb < kQB; ++cb) {
-    const int qi = min(q_wave0 + cb * 32 + l32, nq - 1);
+  // Q^T operand: lane (l32, half) holds query q0 + l32, d = 16 s + 8 half .. +7
+  const int q0 = qt * kBlockQ + wave * kWaveQ;
+  bf16x8 qreg[C::KS];
+  {
+    const int qi = min(q0 + l32, nq - 1);
     const __bf16* qp = q + (int64_t(qi) * heads + head) * D + 8 * half;
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s) qreg[cb][s] = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
+    for (int s = 0; s < C::KS; ++s) qreg[s] = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
   }
 
-  f32x16 o[kQB][C::DB];
+  f32x16 o[C::DB];
 #pragma unroll
-  for (int cb = 0; cb < kQB; ++cb)
+  for (int db = 0; db < C::DB; ++db)
 #pragma unroll
-    for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) o[cb][db][j] = 0.0f;
-  float m_run[kQB], l_run[kQB];
-#pragma unroll
-  for (int cb = 0; cb < kQB; ++cb) {
-    m_run[cb] = -INFINITY;
-    l_run[cb] = 0.0f;
-  }
+    for (int j = 0; j < 16; ++j) o[db][j] = 0.0f;
+  float m_run = -INFINITY;  // running max of scaled logits (log2 units)
+  float l_run = 0.0f;       // this lane's partial sum of probabilities
 
-  // staging map: thread holds keys KPT*g .. KPT*g + KPT-1, d-chunk c
-  const int c_ld = tid % C::CPR;
-  const int g_ld = tid / C::CPR;
-  u32x4 kreg[C::KPT], vreg[C::KPT];
-
-  auto load_tile = [&](int sg, int k0) {
+  // tile copy: 1 KB per wave instruction; lane -> (row, physical chunk)
+  const int cp_row = lane / C::CPR;
+  const int cp_chunk = lane % C::CPR;
+  auto issue_tile = [&](int buf, int sg, int k0) {
     const KvSegment& seg = segs.seg[sg];
-    const __bf16* kb = static_cast<const __bf16*>(seg.k) + head * seg.head_stride + 8 * c_ld;
-    const __bf16* vb = static_cast<const __bf16*>(seg.v) + head * seg.head_stride + 8 * c_ld;
+    const __bf16* kb = static_cast<const __bf16*>(seg.k) + head * seg.head_stride;
+    const __bf16* vb = static_cast<const __bf16*>(seg.v) + head * seg.head_stride;
+    char* base = lds + buf * C::BUF;
 #pragma unroll
-    for (int i = 0; i < C::KPT; ++i) {
-      const int tok = min(k0 + C::KPT * g_ld + i, seg.len - 1);
-      const int64_t off = int64_t(tok) * seg.tok_stride;
-      kreg[i] = *reinterpret_cast<const u32x4*>(kb + off);
-      vreg[i] = *reinterpret_cast<const u32x4*>(vb + off);
+    for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
+      const int blk = wave * C::BLOCKS_PER_WAVE + i;
+      const int r = blk * C::RPB + cp_row;
+      const int tok = min(k0 + r, seg.len - 1);
+      const int64_t off = int64_t(tok) * seg.tok_stride + 8 * (cp_chunk ^ swz(r));
+      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(kb + off), LDS_PTR(void, base + blk * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(vb + off), LDS_PTR(void, base + C::TILE + blk * 1024),
+                                       16, 0, 0);
     }
   };
 
-  auto stage_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < C::KPT; ++i)
-      *reinterpret_cast<u32x4*>(lds_k + (C::KPT * g_ld + i) * C::K_ROW + c_ld * 16) = kreg[i];
-    // V^T: element e of this thread's chunk is d = 8 c + e; its KPT keys are
-    // contiguous in the row at vt_pos(KPT g).
-    const int pos = (C::KPT * g_ld) & ~15;
-    const int p = pos | vt_pos((C::KPT * g_ld) & 15);
-    const int chunk = p >> 3;
-    const int within = (p & 7) * 2;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int d = 8 * c_ld + e;
-      uint16_t h[C::KPT];
-#pragma unroll
-      for (int i = 0; i < C::KPT; ++i) {
-        const uint32_t w = vreg[i][e >> 1];
-        h[i] = (e & 1) ? uint16_t(w >> 16) : uint16_t(w & 0xffff);
-      }
-      char* dst = lds_v + d * C::V_ROW + ((chunk ^ vt_swz(d)) << 4) + within;
-      if constexpr (C::KPT == 4) {
-        u32x2 v2;
-        v2.x = uint32_t(h[0]) | (uint32_t(h[1]) << 16);
-        v2.y = uint32_t(h[2]) | (uint32_t(h[3]) << 16);
-        *reinterpret_cast<u32x2*>(dst) = v2;
-      } else {
-        *reinterpret_cast<uint32_t*>(dst) = uint32_t(h[0]) | (uint32_t(h[1]) << 16);
-      }
-    }
-  };
+  // per-lane LDS offsets of the operand reads
+  // K (A of S^T): row kb*32 + l32, logical chunk 2 ks + half
+  // V (A of O^T, transposing read): lane group g = lane / 16 covers d block
+  //   32 db + 16 (g & 1) and key half (g >> 1); lane l' = lane % 16 reads key
+  //   row kbase + l' / 4 at d offset 4 (l' % 4).
+  const int g = lane >> 4;
+  const int lp = lane & 15;
+  const int v_half = g >> 1;
+  const int v_dsub = 16 * (g & 1) + 4 * (lp & 3);  // d offset within a 32-block
+  const int v_rowin = lp >> 2;
 
-  int sg = 0, k0 = 0;
-  if (segs.n > 0) load_tile(0, 0);
+  int sg = 0, k0 = 0, buf = 0;
+  issue_tile(0, 0, 0);
   while (sg < segs.n) {
     const int len = segs.seg[sg].len;
     const int n_valid = min(kBK, len - k0);
@@ -183,119 +175,110 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       ++nsg;
       nk0 = 0;
     }
-    __syncthreads();  // every wave is done with the previous tile
-    stage_tile();
-    __syncthreads();
-    if (nsg < segs.n) load_tile(nsg, nk0);  // next tile, in flight during this one
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of the current tile have landed
+    __syncthreads();                // everyone's have; everyone is done with the other buffer
+    if (nsg < segs.n) issue_tile(buf ^ 1, nsg, nk0);
+    const char* kt = lds + buf * C::BUF;
+    const char* vt = kt + C::TILE;
 
-    // S^T = K Q^T for the two 32-key blocks
-    f32x16 s[2][kQB];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int cb = 0; cb < kQB; ++cb)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) s[kb][cb][j] = 0.0f;
+    // S^T = K Q^T, two 32-key blocks
+    f32x16 s[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      const char* krow = lds_k + (kb * 32 + l32) * C::K_ROW + half * 16;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) s[kb][j] = 0.0f;
+      const int r = kb * 32 + l32;
+      const char* krow = kt + r * C::ROWB;
+      const int sw = swz(r);
 #pragma unroll
       for (int ks = 0; ks < C::KS; ++ks) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + ks * 32);
-#pragma unroll
-        for (int cb = 0; cb < kQB; ++cb)
-          s[kb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[cb][ks], s[kb][cb], 0, 0, 0);
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + (((2 * ks + half) ^ sw) << 4));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], s[kb], 0, 0, 0);
       }
     }
     if (n_valid < kBK) {
-      // key of register j in block kb: kb*32 + 8*(j/4) + 4*half + j%4
+      // register j of block kb holds key kb*32 + 8 (j / 4) + 4 half + j % 4
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int key = kb * 32 + 8 * (j >> 2) + 4 * half + (j & 3);
-          if (key >= n_valid)
-#pragma unroll
-            for (int cb = 0; cb < kQB; ++cb) s[kb][cb][j] = -INFINITY;
-        }
+        for (int j = 0; j < 16; ++j)
+          if (kb * 32 + 8 * (j >> 2) + 4 * half + (j & 3) >= n_valid) s[kb][j] = -INFINITY;
     }
 
-    // online softmax, one query column per lane (partner lane ^ 32 holds the
-    // other half of the keys)
-    uint32_t pk[2][kQB][8];
+    // online softmax of this lane's query column
+    float mx = s[0][0];
 #pragma unroll
-    for (int cb = 0; cb < kQB; ++cb) {
-      float mx = -INFINITY;
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[kb][cb][j]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[cb], mx * scale_log2);
-      const float alpha = exp2f(m_run[cb] - m_new);
-      m_run[cb] = m_new;
-      float sum = 0.0f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int j = 0; j < 16; j += 2) {
-          const float p0 = exp2f(fmaf(s[kb][cb][j], scale_log2, -m_new));
-          const float p1 = exp2f(fmaf(s[kb][cb][j + 1], scale_log2, -m_new));
-          sum += p0 + p1;
-          pk[kb][cb][j >> 1] = pack_bf16(p0, p1);
-        }
-      l_run[cb] = l_run[cb] * alpha + sum;
+      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[kb][j]);
+    mx = max_across_halves(mx) * scale_log2;
+    if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleThreshold) != 0) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
 #pragma unroll
       for (int db = 0; db < C::DB; ++db)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) o[cb][db][j] *= alpha;
+        for (int j = 0; j < 16; ++j) o[db][j] *= alpha;
     }
+    uint32_t pk[2][8];
+    float sum = 0.0f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int j = 0; j < 16; j += 2) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kb][j], scale_log2, -m_run));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kb][j + 1], scale_log2, -m_run));
+        sum += p0 + p1;
+        pk[kb][j >> 1] = pack_bf16(p0, p1);
+      }
+    l_run += sum;
 
     // O^T += V^T P^T
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int mh = 0; mh < 2; ++mh) {
-        bf16x8 pb[kQB];
-#pragma unroll
-        for (int cb = 0; cb < kQB; ++cb) {
-          u32x4 u = {pk[kb][cb][4 * mh + 0], pk[kb][cb][4 * mh + 1], pk[kb][cb][4 * mh + 2],
-                     pk[kb][cb][4 * mh + 3]};
-          pb[cb] = __builtin_bit_cast(bf16x8, u);
-        }
-        const int chunk = 4 * kb + 2 * mh + half;
+        const u32x4 pu = {pk[kb][4 * mh + 0], pk[kb][4 * mh + 1], pk[kb][4 * mh + 2],
+                          pk[kb][4 * mh + 3]};
+        const bf16x8 pb = __builtin_bit_cast(bf16x8, pu);
+        // keys kbase .. +3 and kbase + 8 .. +11 of this 16-key group
+        const int r0 = kb * 32 + 16 * mh + 4 * v_half + v_rowin;
+        const int r1 = r0 + 8;
 #pragma unroll
         for (int db = 0; db < C::DB; ++db) {
-          const int d = 32 * db + l32;
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(lds_v + d * C::V_ROW +
-                                                           ((chunk ^ vt_swz(d)) << 4));
-#pragma unroll
-          for (int cb = 0; cb < kQB; ++cb)
-            o[cb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[cb], o[cb][db], 0, 0, 0);
+          const int c = (32 * db + v_dsub) >> 3;        // logical chunk
+          const int byte = ((32 * db + v_dsub) & 7) * 2;  // 0 or 8
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              LDS_PTR(s16x4, vt + r0 * C::ROWB + ((c ^ swz(r0)) << 4) + byte));
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              LDS_PTR(s16x4, vt + r1 * C::ROWB + ((c ^ swz(r1)) << 4) + byte));
+          const u32x4 au = {__builtin_bit_cast(u32x2, lo)[0], __builtin_bit_cast(u32x2, lo)[1],
+                            __builtin_bit_cast(u32x2, hi)[0], __builtin_bit_cast(u32x2, hi)[1]};
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, au), pb,
+                                                          o[db], 0, 0, 0);
         }
       }
+    buf ^= 1;
     sg = nsg;
     k0 = nk0;
   }
 
-  // normalise and store: register j of block db holds d = 32 db + 8 (j/4) + 4 half + j%4
+  // normalise and store: register j of block db holds d = 32 db + 8 (j / 4) + 4 half + j % 4
+  const int qi = q0 + l32;
+  const float inv = 1.0f / sum_across_halves(l_run);
+  if (qi < nq) {
+    __bf16* op = out + (int64_t(qi) * heads + head) * D + 4 * half;
 #pragma unroll
-  for (int cb = 0; cb < kQB; ++cb) {
-    const int qi = q_wave0 + cb * 32 + l32;
-    const float l_tot = l_run[cb] + __shfl_xor(l_run[cb], 32);
-    const float inv = 1.0f / l_tot;
-    if (qi < nq) {
-      __bf16* op = out + (int64_t(qi) * heads + head) * D + 4 * half;
+    for (int db = 0; db < C::DB; ++db)
 #pragma unroll
-      for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          u32x2 w;
-          w.x = pack_bf16(o[cb][db][4 * a + 0] * inv, o[cb][db][4 * a + 1] * inv);
-          w.y = pack_bf16(o[cb][db][4 * a + 2] * inv, o[cb][db][4 * a + 3] * inv);
-          *reinterpret_cast<u32x2*>(op + 32 * db + 8 * a) = w;
-        }
-    }
+      for (int a = 0; a < 4; ++a) {
+        u32x2 w;
+        w.x = pack_bf16(o[db][4 * a + 0] * inv, o[db][4 * a + 1] * inv);
+        w.y = pack_bf16(o[db][4 * a + 2] * inv, o[db][4 * a + 3] * inv);
+        *reinterpret_cast<u32x2*>(op + 32 * db + 8 * a) = w;
+      }
   }
 }
 
