@@ -1,18 +1,18 @@
 // bf16 renderer attention on gfx950 matrix cores (flash-attention forward).
 //
-// Work split: a workgroup = 4 waves = 128 queries of one head; each wave owns
-// 32 queries for the whole key loop; two workgroups share a CU, so one's
-// softmax overlaps the other's matrix ops.  Keys arrive as segments (anchor
-// segment, valid history slots, current chunk); each segment is cut into
-// 64-key tiles and only a segment's last tile is partial (its missing keys
-// are masked to -inf): no tile straddles two segments and no empty slot is
-// touched.
+// Work split: a workgroup = 8 waves = 256 queries of one head, one workgroup
+// per CU (two waves per SIMD); each wave owns 32 queries for the whole key
+// loop.  Keys
+// arrive as segments (anchor segment, valid history slots, current chunk);
+// each segment is cut into 64-key tiles and only a segment's last tile is
+// partial (its missing keys are masked to -inf): no tile straddles two
+// segments and no empty slot is touched.
 //
-// Per tile:
+// Products, per 64-key tile:
 //   S^T = K Q^T     v_mfma_f32_32x32x16_bf16; A = K rows read from LDS, B = the
 //                   wave's Q^T, held in registers for the whole loop.
 //   softmax         the accumulator layout of S^T puts one query column in each
-//                   lane (half of the tile's keys; the other half is in lane ^ 32),
+//                   lane (half of a 32-key block; the other half is in lane ^ 32),
 //                   so max and sum are in-lane plus one v_permlane32_swap.  exp2
 //                   with log2(e) folded into the scale.  The running max is only
 //                   raised (and O rescaled) when a column max exceeds it by more
@@ -22,11 +22,18 @@
 //                   transposing LDS read (ds_read_b64_tr_b16); B = P^T, the
 //                   softmax registers rounded to bf16 in place.  The keys of each
 //                   8-key operand are chosen to match the accumulator layout.
+// Software pipeline (besides the second wave on each SIMD, the overlap is built
+// into each wave's instruction stream): while the matrix core computes the first half of
+// S^T of tile t+1, the VALU exponentiates the first half of tile t; while it
+// accumulates that half into O^T, the VALU exponentiates the second half; the
+// second halves of S^T(t+1) and of O^T follow, with the column max of tile t+1.
 // K and V tiles are copied from HBM straight into LDS (global_load_lds_dwordx4,
-// 16 bytes per lane) one tile ahead, into a double buffer: one barrier per
-// tile.  Tile rows are stored without padding, with an XOR swizzle of their
-// 16-byte chunks that keeps both the K reads and the transposing V reads free
-// of bank conflicts.
+// 16 bytes per lane) two tiles ahead, into a ring of three tile slots: one
+// barrier per tile.  The loop is unrolled by three so every slot reference is
+// static (reads of one slot are never ordered behind the copy into another).
+// Tile rows are stored without padding, with an XOR swizzle of their 16-byte
+// chunks that keeps both the K reads and the transposing V reads free of bank
+// conflicts on the 64-bank LDS.
 // Workgroups are renumbered so that consecutive Q tiles of one head land on
 // the same XCD (the hardware deals workgroups to the 8 XCDs round robin) and
 // share that XCD's L2 for the head's K/V.
@@ -51,9 +58,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
 #define GLOBAL_PTR(p) ((const __attribute__((address_space(1))) void*)(p))
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kWaveQ = 32;                  // queries per wave
+constexpr int kCB = 1;                      // 32-query column blocks per wave
+constexpr int kWaveQ = 32 * kCB;            // queries per wave
 constexpr int kBlockQ = kWaves * kWaveQ;    // queries per workgroup
 constexpr int kBK = 64;                     // keys per tile
 constexpr int kXcds = 8;
@@ -69,14 +77,23 @@ struct Cfg {
   static constexpr int BLOCKS = kBK / RPB;   // 1 KB copies per tile (per tensor)
   static constexpr int BLOCKS_PER_WAVE = BLOCKS / kWaves;
   static constexpr int TILE = kBK * ROWB;    // bytes of one K (or V) tile
-  static constexpr int BUF = 2 * TILE;       // K tile then V tile
+  static constexpr int SLOT = 2 * TILE;      // K tile then V tile
+  static_assert(BLOCKS % kWaves == 0, "every wave copies the same number of 1 KB blocks");
 };
 
-// XOR swizzle of the 16-byte chunks of tile row r: over any 8 consecutive rows
-// it is a permutation of 0..7 (K reads: 32 rows, one chunk), and over any 4
-// rows starting at a multiple of 4 its halves are distinct (V transposing
-// reads: 4 rows x 2 adjacent chunks).
-__device__ inline int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+// XOR swizzle of the 16-byte chunks of tile row r, for an LDS that serves
+// 256 bytes per clock (64 banks): a 16-lane quarter of a 16-byte K read (16
+// consecutive rows, one chunk) and a 32-lane half of an 8-byte transposing V
+// read (4 rows x 4 adjacent chunks) must each touch 16 (resp. 32) distinct
+// 16-byte (8-byte) bank slots.  d = 128 (256-byte rows, 16 chunks): the row's
+// low two bits pick the chunk group and the next two the chunk inside it.
+// d = 64 (128-byte rows, 8 chunks, two rows per bank line): same idea on the
+// row bits above the line parity.
+template <int D>
+__device__ inline int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
 
 __device__ inline uint32_t pack_bf16(float a, float b) {
   f32x2 f = {a, b};
@@ -93,12 +110,19 @@ __device__ inline float sum_across_halves(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Tile cursor over the key segments: tile = (segment, first key).
+struct Cursor {
+  int sg, k0;
+};
+
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, int nq, int heads,
                       float scale_log2, KvSegments segs, int n_qtiles) {
   using C = Cfg<D>;
-  __shared__ __attribute__((aligned(1024))) char lds[2 * C::BUF];
+  __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
+  __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
+  __shared__ __attribute__((aligned(1024))) char lds2[C::SLOT];
 
   // XCD-aware renumbering: hardware block b runs on XCD b % 8; give each XCD a
   // contiguous range of logical tiles.
@@ -116,169 +140,264 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   const int l32 = lane & 31;
   const int half = lane >> 5;
 
-  // Q^T operand: lane (l32, half) holds query q0 + l32, d = 16 s + 8 half .. +7
+  // Q^T operand: lane (l32, half) of column block cb holds query
+  // q0 + 32 cb + l32, elements d = 16 s + 8 half .. +7 of slice s.
   const int q0 = qt * kBlockQ + wave * kWaveQ;
-  bf16x8 qreg[C::KS];
-  {
-    const int qi = min(q0 + l32, nq - 1);
+  bf16x8 qreg[kCB][C::KS];
+#pragma unroll
+  for (int cb = 0; cb < kCB; ++cb) {
+    const int qi = min(q0 + 32 * cb + l32, nq - 1);
     const __bf16* qp = q + (int64_t(qi) * heads + head) * D + 8 * half;
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s) qreg[s] = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
+    for (int s = 0; s < C::KS; ++s) qreg[cb][s] = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
   }
 
-  f32x16 o[C::DB];
+  f32x16 o[kCB][C::DB];
 #pragma unroll
-  for (int db = 0; db < C::DB; ++db)
+  for (int cb = 0; cb < kCB; ++cb)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) o[db][j] = 0.0f;
-  float m_run = -INFINITY;  // running max of scaled logits (log2 units)
-  float l_run = 0.0f;       // this lane's partial sum of probabilities
+    for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) o[cb][db][j] = 0.0f;
+  float m_run[kCB], l_run[kCB];
+#pragma unroll
+  for (int cb = 0; cb < kCB; ++cb) {
+    m_run[cb] = -INFINITY;  // running max of scaled logits (log2 units)
+    l_run[cb] = 0.0f;       // this lane's partial sum of probabilities
+  }
+
+  // number of tiles
+  int n_tiles = 0;
+  for (int i = 0; i < segs.n; ++i) n_tiles += (segs.seg[i].len + kBK - 1) / kBK;
+  auto advance = [&](Cursor c) {
+    c.k0 += kBK;
+    if (c.k0 >= segs.seg[c.sg].len) {
+      ++c.sg;
+      c.k0 = 0;
+    }
+    return c;
+  };
 
   // tile copy: 1 KB per wave instruction; lane -> (row, physical chunk)
   const int cp_row = lane / C::CPR;
   const int cp_chunk = lane % C::CPR;
-  auto issue_tile = [&](int buf, int sg, int k0) {
-    const KvSegment& seg = segs.seg[sg];
+  auto issue_tile = [&](char* base, Cursor c) {
+    const KvSegment& seg = segs.seg[c.sg];
     const __bf16* kb = static_cast<const __bf16*>(seg.k) + head * seg.head_stride;
     const __bf16* vb = static_cast<const __bf16*>(seg.v) + head * seg.head_stride;
-    char* base = lds + buf * C::BUF;
 #pragma unroll
     for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
       const int blk = wave * C::BLOCKS_PER_WAVE + i;
       const int r = blk * C::RPB + cp_row;
-      const int tok = min(k0 + r, seg.len - 1);
-      const int64_t off = int64_t(tok) * seg.tok_stride + 8 * (cp_chunk ^ swz(r));
+      const int tok = min(c.k0 + r, seg.len - 1);
+      const int64_t off = int64_t(tok) * seg.tok_stride + 8 * (cp_chunk ^ swz<D>(r));
       __builtin_amdgcn_global_load_lds(GLOBAL_PTR(kb + off), LDS_PTR(void, base + blk * 1024), 16, 0, 0);
       __builtin_amdgcn_global_load_lds(GLOBAL_PTR(vb + off), LDS_PTR(void, base + C::TILE + blk * 1024),
                                        16, 0, 0);
     }
   };
 
-  // per-lane LDS offsets of the operand reads
-  // K (A of S^T): row kb*32 + l32, logical chunk 2 ks + half
-  // V (A of O^T, transposing read): lane group g = lane / 16 covers d block
-  //   32 db + 16 (g & 1) and key half (g >> 1); lane l' = lane % 16 reads key
-  //   row kbase + l' / 4 at d offset 4 (l' % 4).
+  // LDS read addresses.  The swizzle only flips chunk bits that the row offset
+  // leaves clear, so each read is (slot + immediate) + (lane base ^ constant):
+  //   K (A of S^T), row kb*32 + l32, chunk 2 ks + half: k_lane ^ (ks << 5), +8 KB for kb = 1
+  //     (both blocks share the swizzle: it depends on the row's low four bits only);
+  //   V (A of O^T, transposing read), lane group g = lane / 16 covers d block
+  //     32 db + 16 (g & 1) and key half (g >> 1); lane l' = lane % 16 reads key row
+  //     kbase + l' / 4 at d offset 4 (l' % 4): v_lane[lo/hi] ^ (db << 6) for D = 128
+  //     (chunk group = db), + (32 kb + 16 mh) rows.
+  int k_lane = l32 * C::ROWB + ((half ^ swz<D>(l32)) << 4);
   const int g = lane >> 4;
   const int lp = lane & 15;
-  const int v_half = g >> 1;
-  const int v_dsub = 16 * (g & 1) + 4 * (lp & 3);  // d offset within a 32-block
-  const int v_rowin = lp >> 2;
+  const int v_row = 4 * (g >> 1) + (lp >> 2);               // row of the lo read within a 16-key group
+  const int v_dsub = 16 * (g & 1) + 4 * (lp & 3);            // d offset within a 32-d block
+  int v_lane[2];
+#pragma unroll
+  for (int hi = 0; hi < 2; ++hi) {
+    const int r = v_row + 8 * hi;
+    v_lane[hi] = r * C::ROWB + (((v_dsub >> 3) ^ swz<D>(r)) << 4) + (v_dsub & 7) * 2;
+  }
+  // chunk bits flipped per d block: D = 128 has 4 chunks per 32-d block, D = 64 as well
+  constexpr int kVdbShift = 6;   // (4 chunks per db) << 4 bytes
 
-  int sg = 0, k0 = 0, buf = 0;
-  issue_tile(0, 0, 0);
-  while (sg < segs.n) {
-    const int len = segs.seg[sg].len;
-    const int n_valid = min(kBK, len - k0);
-    int nsg = sg, nk0 = k0 + kBK;
-    if (nk0 >= len) {
-      ++nsg;
-      nk0 = 0;
+  // S^T of 32-key block kb of a tile into s[kb][cb], both column blocks
+  auto compute_s = [&](const char* kt, int kb, f32x16 (&s)[2][kCB]) {
+#pragma unroll
+    for (int cb = 0; cb < kCB; ++cb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) s[kb][cb][j] = 0.0f;
+    const char* kbase = kt + kb * 32 * C::ROWB;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kbase + (k_lane ^ (ks << 5)));
+#pragma unroll
+      for (int cb = 0; cb < kCB; ++cb)
+        s[kb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[cb][ks], s[kb][cb], 0, 0, 0);
     }
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of the current tile have landed
-    __syncthreads();                // everyone's have; everyone is done with the other buffer
-    if (nsg < segs.n) issue_tile(buf ^ 1, nsg, nk0);
-    const char* kt = lds + buf * C::BUF;
-    const char* vt = kt + C::TILE;
+  };
 
-    // S^T = K Q^T, two 32-key blocks
-    f32x16 s[2];
+  // mask keys >= n_valid of a partial tile (register j of block kb holds key
+  // kb*32 + 8 (j / 4) + 4 half + j % 4)
+  auto mask_s = [&](f32x16 (&s)[2][kCB], int n_valid) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) s[kb][j] = 0.0f;
-      const int r = kb * 32 + l32;
-      const char* krow = kt + r * C::ROWB;
-      const int sw = swz(r);
+      for (int j = 0; j < 16; ++j)
+        if (kb * 32 + 8 * (j >> 2) + 4 * half + (j & 3) >= n_valid)
 #pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + (((2 * ks + half) ^ sw) << 4));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], s[kb], 0, 0, 0);
-      }
-    }
-    if (n_valid < kBK) {
-      // register j of block kb holds key kb*32 + 8 (j / 4) + 4 half + j % 4
+          for (int cb = 0; cb < kCB; ++cb) s[kb][cb][j] = -INFINITY;
+  };
+
+  // column max of a tile; raise the running max (and rescale O) when it grows
+  // by more than the threshold
+  auto update_max = [&](const f32x16 (&s)[2][kCB]) {
+#pragma unroll
+    for (int cb = 0; cb < kCB; ++cb) {
+      float mx = s[0][cb][0];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (kb * 32 + 8 * (j >> 2) + 4 * half + (j & 3) >= n_valid) s[kb][j] = -INFINITY;
+        for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[kb][cb][j]);
+      mx = max_across_halves(mx) * scale_log2;
+      if (__builtin_amdgcn_ballot_w64(mx > m_run[cb] + kRescaleThreshold) != 0) {
+        const float m_new = fmaxf(m_run[cb], mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run[cb] - m_new);
+        m_run[cb] = m_new;
+        l_run[cb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) o[cb][db][j] *= alpha;
+      }
     }
+  };
 
-    // online softmax of this lane's query column
-    float mx = s[0][0];
+  // probabilities of 32-key block kb, both column blocks, as packed bf16
+  auto probs = [&](const f32x16 (&s)[2][kCB], int kb, uint32_t (&pk)[kCB][8]) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[kb][j]);
-    mx = max_across_halves(mx) * scale_log2;
-    if (__builtin_amdgcn_ballot_w64(mx > m_run + kRescaleThreshold) != 0) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) o[db][j] *= alpha;
-    }
-    uint32_t pk[2][8];
-    float sum = 0.0f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int cb = 0; cb < kCB; ++cb) {
+      float sum = 0.0f;
 #pragma unroll
       for (int j = 0; j < 16; j += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kb][j], scale_log2, -m_run));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kb][j + 1], scale_log2, -m_run));
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kb][cb][j], scale_log2, -m_run[cb]));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kb][cb][j + 1], scale_log2, -m_run[cb]));
         sum += p0 + p1;
-        pk[kb][j >> 1] = pack_bf16(p0, p1);
+        pk[cb][j >> 1] = pack_bf16(p0, p1);
       }
-    l_run += sum;
+      l_run[cb] += sum;
+    }
+  };
 
-    // O^T += V^T P^T
+  // O^T += V^T P^T for 32-key block kb
+  auto pv = [&](const char* vt, int kb, const uint32_t (&pk)[kCB][8]) {
+#pragma unroll
+    for (int mh = 0; mh < 2; ++mh) {
+      bf16x8 pb[kCB];
+#pragma unroll
+      for (int cb = 0; cb < kCB; ++cb) {
+        const u32x4 pu = {pk[cb][4 * mh + 0], pk[cb][4 * mh + 1], pk[cb][4 * mh + 2],
+                          pk[cb][4 * mh + 3]};
+        pb[cb] = __builtin_bit_cast(bf16x8, pu);
+      }
+      const char* vbase = vt + (kb * 32 + 16 * mh) * C::ROWB;
+#pragma unroll
+      for (int db = 0; db < C::DB; ++db) {
+        // keys kbase .. +3 (lo) and kbase + 8 .. +11 (hi) of this 16-key group
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            LDS_PTR(s16x4, vbase + (v_lane[0] ^ (db << kVdbShift))));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            LDS_PTR(s16x4, vbase + (v_lane[1] ^ (db << kVdbShift))));
+        const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
+        const u32x4 au = {lo2[0], lo2[1], hi2[0], hi2[1]};
+        const bf16x8 a = __builtin_bit_cast(bf16x8, au);
+#pragma unroll
+        for (int cb = 0; cb < kCB; ++cb)
+          o[cb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[cb], o[cb][db], 0, 0, 0);
+      }
+    }
+  };
+
+  // ---- prologue: tiles 0 and 1 in flight, S^T of tile 0 -----------------------------
+  Cursor c_next = {0, 0};                    // the tile whose S^T the iteration computes
+  Cursor c_dma = advance(c_next);            // the tile the iteration copies
+  issue_tile(lds0, c_next);
+  if (n_tiles > 1) {
+    issue_tile(lds1, c_dma);
+    c_dma = advance(c_dma);                  // tile 2
+  }
+  f32x16 s_cur[2][kCB];
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  compute_s(lds0, 0, s_cur);
+  compute_s(lds0, 1, s_cur);
+  {
+    const int nv = min(kBK, segs.seg[0].len);
+    if (nv < kBK) mask_s(s_cur, nv);
+  }
+  update_max(s_cur);
+  c_next = advance(c_next);                  // tile 1
+
+  // ---- main loop: iteration t finishes tile t and computes S^T of tile t+1 -----------
+  // tile t sits in slot t % 3: its V is read from v_slot, the K of tile t+1 from
+  // k_slot, and tile t+2 is copied into dma_slot (tile t-1's, free after the barrier).
+  auto iteration = [&](int t, char* v_slot, char* k_slot, char* dma_slot) {
+    const bool has_next = t + 1 < n_tiles;
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of tile t+1 have landed
+    __syncthreads();                // everyone's have; everyone is done with tile t-1
+    if (t + 2 < n_tiles) issue_tile(dma_slot, c_dma);
+    // keep the per-read address arithmetic inside the loop (no hoisted copies)
+    asm volatile("" : "+v"(k_lane), "+v"(v_lane[0]), "+v"(v_lane[1]));
+    // (past the last tile the S^T products read a stale slot and are discarded)
+    f32x16 s_nxt[2][kCB];
+    uint32_t pk0[kCB][8], pk1[kCB][8];
+    // block 0 of S^T(t+1) on the matrix core while the VALU exponentiates block 0 of tile t
+    compute_s(k_slot, 0, s_nxt);
+    probs(s_cur, 0, pk0);
+    // block 0 of tile t into O^T while the VALU exponentiates block 1 of tile t
+    pv(v_slot + C::TILE, 0, pk0);
+    probs(s_cur, 1, pk1);
+    // block 1 of S^T(t+1), then block 1 of tile t into O^T, while the VALU takes
+    // the column max of tile t+1
+    compute_s(k_slot, 1, s_nxt);
+    pv(v_slot + C::TILE, 1, pk1);
+    if (has_next) {
+      const int nv = min(kBK, segs.seg[c_next.sg].len - c_next.k0);
+      if (nv < kBK) mask_s(s_nxt, nv);
+      update_max(s_nxt);
+    }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int mh = 0; mh < 2; ++mh) {
-        const u32x4 pu = {pk[kb][4 * mh + 0], pk[kb][4 * mh + 1], pk[kb][4 * mh + 2],
-                          pk[kb][4 * mh + 3]};
-        const bf16x8 pb = __builtin_bit_cast(bf16x8, pu);
-        // keys kbase .. +3 and kbase + 8 .. +11 of this 16-key group
-        const int r0 = kb * 32 + 16 * mh + 4 * v_half + v_rowin;
-        const int r1 = r0 + 8;
-#pragma unroll
-        for (int db = 0; db < C::DB; ++db) {
-          const int c = (32 * db + v_dsub) >> 3;        // logical chunk
-          const int byte = ((32 * db + v_dsub) & 7) * 2;  // 0 or 8
-          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              LDS_PTR(s16x4, vt + r0 * C::ROWB + ((c ^ swz(r0)) << 4) + byte));
-          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              LDS_PTR(s16x4, vt + r1 * C::ROWB + ((c ^ swz(r1)) << 4) + byte));
-          const u32x4 au = {__builtin_bit_cast(u32x2, lo)[0], __builtin_bit_cast(u32x2, lo)[1],
-                            __builtin_bit_cast(u32x2, hi)[0], __builtin_bit_cast(u32x2, hi)[1]};
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, au), pb,
-                                                          o[db], 0, 0, 0);
-        }
-      }
-    buf ^= 1;
-    sg = nsg;
-    k0 = nk0;
+      for (int cb = 0; cb < kCB; ++cb) s_cur[kb][cb] = s_nxt[kb][cb];
+    if (has_next) c_next = advance(c_next);
+    if (t + 2 < n_tiles) c_dma = advance(c_dma);
+  };
+
+  for (int t = 0; t < n_tiles;) {
+    iteration(t, lds0, lds1, lds2);
+    if (++t >= n_tiles) break;
+    iteration(t, lds1, lds2, lds0);
+    if (++t >= n_tiles) break;
+    iteration(t, lds2, lds0, lds1);
+    ++t;
   }
 
   // normalise and store: register j of block db holds d = 32 db + 8 (j / 4) + 4 half + j % 4
-  const int qi = q0 + l32;
-  const float inv = 1.0f / sum_across_halves(l_run);
-  if (qi < nq) {
-    __bf16* op = out + (int64_t(qi) * heads + head) * D + 4 * half;
 #pragma unroll
-    for (int db = 0; db < C::DB; ++db)
+  for (int cb = 0; cb < kCB; ++cb) {
+    const int qi = q0 + 32 * cb + l32;
+    const float inv = 1.0f / sum_across_halves(l_run[cb]);
+    if (qi < nq) {
+      __bf16* op = out + (int64_t(qi) * heads + head) * D + 4 * half;
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        u32x2 w;
-        w.x = pack_bf16(o[db][4 * a + 0] * inv, o[db][4 * a + 1] * inv);
-        w.y = pack_bf16(o[db][4 * a + 2] * inv, o[db][4 * a + 3] * inv);
-        *reinterpret_cast<u32x2*>(op + 32 * db + 8 * a) = w;
-      }
+      for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          u32x2 w;
+          w.x = pack_bf16(o[cb][db][4 * a + 0] * inv, o[cb][db][4 * a + 1] * inv);
+          w.y = pack_bf16(o[cb][db][4 * a + 2] * inv, o[cb][db][4 * a + 3] * inv);
+          *reinterpret_cast<u32x2*>(op + 32 * db + 8 * a) = w;
+        }
+    }
   }
 }
 
