@@ -110,6 +110,15 @@ __device__ inline float sum_across_halves(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// 64-bit value of lane `lane` (wave-uniform index).  The builtin works on
+// signed 32-bit words: each half is widened as unsigned, so a low word with
+// its top bit set does not sign-extend into the high word.
+__device__ inline uint64_t readlane_u64(uint64_t v, int lane) {
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), lane));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v >> 32)), lane));
+  return (uint64_t(hi) << 32) | uint64_t(lo);
+}
+
 // Tile cursor over the key segments: tile = (segment, first key).
 struct Cursor {
   int sg, k0;
@@ -166,34 +175,62 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     l_run[cb] = 0.0f;       // this lane's partial sum of probabilities
   }
 
+  // Segment table in registers: lane i holds segment i's length, tokens-stride
+  // (bytes) and the byte addresses of this head's K and V rows.  Inside the
+  // loop a field of segment sg is read with v_readlane: no scalar memory loads
+  // there, so the LDS-read counter waits can stay partial.
+  int sg_len = 0;
+  uint32_t sg_row_bytes = 0;
+  uint64_t sg_k = 0, sg_v = 0;
+#pragma unroll
+  for (int i = 0; i < kMaxSegments; ++i)
+    if (lane == i && i < segs.n) {
+      const KvSegment& sgi = segs.seg[i];
+      sg_len = sgi.len;
+      sg_row_bytes = 2u * uint32_t(sgi.tok_stride);
+      sg_k = reinterpret_cast<uint64_t>(sgi.k) + 2ull * uint64_t(head) * uint64_t(sgi.head_stride);
+      sg_v = reinterpret_cast<uint64_t>(sgi.v) + 2ull * uint64_t(head) * uint64_t(sgi.head_stride);
+    }
+  auto seg_len = [&](int i) { return __builtin_amdgcn_readlane(sg_len, i); };
+
   // number of tiles
   int n_tiles = 0;
-  for (int i = 0; i < segs.n; ++i) n_tiles += (segs.seg[i].len + kBK - 1) / kBK;
+  for (int i = 0; i < segs.n; ++i) n_tiles += (seg_len(i) + kBK - 1) / kBK;
   auto advance = [&](Cursor c) {
     c.k0 += kBK;
-    if (c.k0 >= segs.seg[c.sg].len) {
+    if (c.k0 >= seg_len(c.sg)) {
       ++c.sg;
       c.k0 = 0;
     }
     return c;
   };
 
-  // tile copy: 1 KB per wave instruction; lane -> (row, physical chunk)
-  const int cp_row = lane / C::CPR;
-  const int cp_chunk = lane % C::CPR;
+  // tile copy: 1 KB per wave instruction; lane -> (row, physical chunk).  A
+  // segment's rows are at most 2^31 bytes apart (the host limits a chunk to
+  // 2^31 elements), so each lane's source is a 32-bit byte offset from the
+  // segment's (uniform) head base; rows past a partial tile's end re-read its
+  // last row, whose scores are masked.
+  int cp_row[C::BLOCKS_PER_WAVE], cp_choff[C::BLOCKS_PER_WAVE];
+#pragma unroll
+  for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
+    const int r = (wave * C::BLOCKS_PER_WAVE + i) * C::RPB + lane / C::CPR;
+    cp_row[i] = r;
+    cp_choff[i] = 16 * ((lane % C::CPR) ^ swz<D>(r));
+  }
   auto issue_tile = [&](char* base, Cursor c) {
-    const KvSegment& seg = segs.seg[c.sg];
-    const __bf16* kb = static_cast<const __bf16*>(seg.k) + head * seg.head_stride;
-    const __bf16* vb = static_cast<const __bf16*>(seg.v) + head * seg.head_stride;
+    const int len = seg_len(c.sg);
+    const uint32_t row_bytes = uint32_t(__builtin_amdgcn_readlane(int(sg_row_bytes), c.sg));
+    const char* kb = reinterpret_cast<const char*>(readlane_u64(sg_k, c.sg));
+    const char* vb = reinterpret_cast<const char*>(readlane_u64(sg_v, c.sg));
+    const bool partial = c.k0 + kBK > len;
 #pragma unroll
     for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
-      const int blk = wave * C::BLOCKS_PER_WAVE + i;
-      const int r = blk * C::RPB + cp_row;
-      const int tok = min(c.k0 + r, seg.len - 1);
-      const int64_t off = int64_t(tok) * seg.tok_stride + 8 * (cp_chunk ^ swz<D>(r));
-      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(kb + off), LDS_PTR(void, base + blk * 1024), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(vb + off), LDS_PTR(void, base + C::TILE + blk * 1024),
-                                       16, 0, 0);
+      int tok = c.k0 + cp_row[i];
+      if (partial) tok = min(tok, len - 1);
+      const uint32_t off = uint32_t(tok) * row_bytes + uint32_t(cp_choff[i]);
+      char* dst = base + (wave * C::BLOCKS_PER_WAVE + i) * 1024;
+      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(kb + off), LDS_PTR(void, dst), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(vb + off), LDS_PTR(void, dst + C::TILE), 16, 0, 0);
     }
   };
 
@@ -330,7 +367,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   compute_s(lds0, 0, s_cur);
   compute_s(lds0, 1, s_cur);
   {
-    const int nv = min(kBK, segs.seg[0].len);
+    const int nv = min(kBK, seg_len(0));
     if (nv < kBK) mask_s(s_cur, nv);
   }
   update_max(s_cur);
@@ -360,7 +397,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     compute_s(k_slot, 1, s_nxt);
     pv(v_slot + C::TILE, 1, pk1);
     if (has_next) {
-      const int nv = min(kBK, segs.seg[c_next.sg].len - c_next.k0);
+      const int nv = min(kBK, seg_len(c_next.sg) - c_next.k0);
       if (nv < kBK) mask_s(s_nxt, nv);
       update_max(s_nxt);
     }
