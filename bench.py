@@ -12,12 +12,19 @@ Infinity Cache does not hold the previous layer's data.
 
 Prints one JSON line.  `value` is attention TFLOP/s over the whole timed
 region (attention FLOPs of every step / wall time of the steps, RoPE and
-publish included); the per-kernel breakdown, the roofline of the attention
-kernel and the CPU oracle baseline are attached.
+publish included).  Events recorded between the launches of every layer inside
+the timed region give each kernel's average launch duration, from which the
+roofline of the attention kernel is taken; its HBM traffic comes from the
+counter summary under profiles/ when that summary was taken on the current
+kernel source.  The CPU oracle baseline is attached.
+
+`--copy-calibration` instead runs only a plain device copy of 1 GiB three
+times: the reference dispatch that scales the FETCH_SIZE / WRITE_SIZE counters.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -37,6 +44,7 @@ from paper_2609_32540_amd import ff  # noqa: E402
 METRIC = "attention TFLOP/s + ms per chunk-stage forward (attn+publish), % bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak (published)
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E (published)
+ATTN_SOURCE = os.path.join(ROOT, "paper_2609_32540_amd", "csrc", "attn_bf16.hip")
 
 
 def log(msg: str) -> None:
@@ -118,6 +126,41 @@ class Workspace:
         return self.attn_flops(chunk) * w.layers
 
 
+def measured_traffic(workload: str):
+    """HBM bytes per attention launch from the committed counter summary.
+
+    The summary holds a JSON block with the SHA-256 of the kernel source the
+    counters were taken on; a summary of another source gives None.
+    """
+    path = os.path.join(ROOT, "profiles", f"attn_bf16_{workload}_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    text = open(path).read()
+    try:
+        block = text.split("```json", 1)[1].split("```", 1)[0]
+        rec = json.loads(block)
+    except (IndexError, ValueError):
+        return None, "unreadable counter summary"
+    sha = hashlib.sha256(open(ATTN_SOURCE, "rb").read()).hexdigest()
+    if rec.get("kernel_source_sha256") != sha:
+        return None, "kernel changed since the counters were taken"
+    return float(rec["hbm_bytes_per_launch"]), os.path.relpath(path, ROOT)
+
+
+def copy_calibration() -> int:
+    """Three device-to-device copies of 1 GiB (2**28 float32), nothing else."""
+    n = 2 ** 28
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": 4 * n, "copy_calibration_bytes_written": 4 * n,
+                      "copies": 3}), flush=True)
+    return 0
+
+
 def cpu_baseline(w: synth.Workload, target_s: float = 12.0) -> dict:
     """The float64 oracle's attention on 1-head x 512-query slices at the full key length."""
     from oracle import ff_oracle as fo
@@ -159,7 +202,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=8)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="14b-720p", choices=sorted(synth.WORKLOADS))
-    ap.add_argument("--breakdown-steps", type=int, default=4)
+    ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     args = ap.parse_args()
@@ -170,6 +213,8 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
+    if args.copy_calibration:
+        return copy_calibration()
     w = synth.WORKLOADS[args.workload]
     if w.dtype != "bf16":
         print("the benchmark workloads are the bf16 ones", file=sys.stderr)
@@ -187,13 +232,19 @@ def main() -> int:
     torch.cuda.synchronize()
     log("warmup done")
 
-    # timed region: K steps bracketed by events on the launch stream
+    # timed region: K steps bracketed by events on the launch stream, with
+    # events between the kernels of every layer for the per-kernel durations
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    events, chunks = [], []
+    for _ in range(args.steps):
+        events.append([[torch.cuda.Event(enable_timing=True) for _ in range(4)]
+                       for _ in range(w.layers)])
     flops = 0.0
     torch.cuda.synchronize()
     start.record(stream)
-    for _ in range(args.steps):
-        flops += ws.step()
+    for k in range(args.steps):
+        chunks.append(ws.next[0])
+        flops += ws.step(events[k])
     stop.record(stream)
     torch.cuda.synchronize()
     ms_total = start.elapsed_time(stop)
@@ -201,19 +252,14 @@ def main() -> int:
     value = flops / (ms_total * 1e-3) / 1e12
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {value:.1f} TFLOP/s")
 
-    # per-kernel breakdown: events between the launches of each layer
-    bd_steps = max(1, args.breakdown_steps)
     rope_ms, attn_ms, pub_ms, attn_flops = [], [], [], []
-    for _ in range(bd_steps):
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(w.layers)]
-        chunk = ws.next[0]
-        ws.step(ev)
-        torch.cuda.synchronize()
+    for k in range(args.steps):
         for l in range(w.layers):
-            rope_ms.append(ev[l][0].elapsed_time(ev[l][1]))
-            attn_ms.append(ev[l][1].elapsed_time(ev[l][2]))
-            pub_ms.append(ev[l][2].elapsed_time(ev[l][3]))
-            attn_flops.append(ws.attn_flops(chunk))
+            ev = events[k][l]
+            rope_ms.append(ev[0].elapsed_time(ev[1]))
+            attn_ms.append(ev[1].elapsed_time(ev[2]))
+            pub_ms.append(ev[2].elapsed_time(ev[3]))
+            attn_flops.append(ws.attn_flops(chunks[k]))
     attn_avg = float(np.mean(attn_ms))
     pub_avg = float(np.mean(pub_ms))
     rope_avg = float(np.mean(rope_ms))
@@ -226,6 +272,10 @@ def main() -> int:
     log(f"attention {attn_avg:.3f} ms/launch = {attn_achieved:.1f} TFLOP/s; publish {pub_avg*1e3:.1f} us "
         f"= {pub_gbs:.0f} GB/s; rope {rope_avg*1e3:.1f} us = {rope_gbs:.0f} GB/s")
 
+    traffic, traffic_src = measured_traffic(w.name)
+    # compulsory bytes of one launch: Q, K, V, O of the chunk once each, every
+    # history and anchor key/value once (the whole read set, all heads)
+    attn_bytes = elem * w.heads * w.head_dim * (2 * w.chunk_tokens + 2 * ws.kv_tokens(chunks[-1]))
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -256,7 +306,9 @@ def main() -> int:
         },
         "roofline": {"bound": "mfma", "achieved": round(attn_achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": traffic, "traffic_unit": "HBM bytes per launch",
+                     "traffic_source": traffic_src,
+                     "algorithmic_bytes_per_launch": attn_bytes},
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
