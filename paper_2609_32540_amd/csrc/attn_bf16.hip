@@ -28,8 +28,8 @@
 // accumulates that half into O^T, the VALU exponentiates the second half; the
 // second halves of S^T(t+1) and of O^T follow, with the column max of tile t+1.
 // K and V tiles are copied from HBM straight into LDS (global_load_lds_dwordx4,
-// 16 bytes per lane) two tiles ahead, into a ring of three tile slots: one
-// barrier per tile.  The loop is unrolled by three so every slot reference is
+// 16 bytes per lane, issued by waves 0-3) two tiles ahead, into a ring of three
+// tile slots: one barrier per tile.  The loop is unrolled by three so every slot reference is
 // static (reads of one slot are never ordered behind the copy into another).
 // Tile rows are stored without padding, with an XOR swizzle of their 16-byte
 // chunks that keeps both the K reads and the transposing V reads free of bank
@@ -66,6 +66,10 @@ constexpr int kBlockQ = kWaves * kWaveQ;    // queries per workgroup
 constexpr int kBK = 64;                     // keys per tile
 constexpr int kXcds = 8;
 constexpr float kRescaleThreshold = 8.0f;   // log2 units
+// Waves w and w + 4 share a SIMD and the issue arbiter favours the older one
+// (w < 4), which reaches each tile's barrier well ahead of its partner; the
+// tile copies are therefore all issued by waves 0-3, off the partner's path.
+constexpr int kCopyWaves = kWaves / 2;
 
 template <int D>
 struct Cfg {
@@ -75,10 +79,10 @@ struct Cfg {
   static constexpr int CPR = D / 8;          // 16-byte chunks per row
   static constexpr int RPB = 1024 / ROWB;    // rows per 1 KB wave copy
   static constexpr int BLOCKS = kBK / RPB;   // 1 KB copies per tile (per tensor)
-  static constexpr int BLOCKS_PER_WAVE = BLOCKS / kWaves;
+  static constexpr int BLOCKS_PER_WAVE = BLOCKS / kCopyWaves;   // copies by waves 0 .. kCopyWaves-1
   static constexpr int TILE = kBK * ROWB;    // bytes of one K (or V) tile
   static constexpr int SLOT = 2 * TILE;      // K tile then V tile
-  static_assert(BLOCKS % kWaves == 0, "every wave copies the same number of 1 KB blocks");
+  static_assert(BLOCKS % kCopyWaves == 0, "every copying wave copies the same number of 1 KB blocks");
 };
 
 // XOR swizzle of the 16-byte chunks of tile row r, for an LDS that serves
@@ -218,6 +222,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     cp_choff[i] = 16 * ((lane % C::CPR) ^ swz<D>(r));
   }
   auto issue_tile = [&](char* base, Cursor c) {
+    if (wave >= kCopyWaves) return;
     const int len = seg_len(c.sg);
     const uint32_t row_bytes = uint32_t(__builtin_amdgcn_readlane(int(sg_row_bytes), c.sg));
     const char* kb = reinterpret_cast<const char*>(readlane_u64(sg_k, c.sg));
