@@ -147,6 +147,51 @@ def measured_traffic(workload: str):
     return float(rec["hbm_bytes_per_launch"]), os.path.relpath(path, ROOT)
 
 
+def packed_clip(w: synth.Workload, reps: int = 3) -> dict:
+    """ff_packed_attention over the workload's whole clip at one stage and layer.
+
+    Q, K, V of all chunks in one token-major array, the anchor frames of
+    every window in another; chunk i sees its window Gamma(i) and chunks
+    max(0, i - W) .. i.  Seeded N(0,1) inputs drawn on the device.
+    """
+    dev = torch.device("cuda", 0)
+    n, Nq, G = w.n_chunks, w.chunk_tokens, w.tokens_per_frame
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    shape = (n * Nq, w.heads, w.head_dim)
+    q, k, v = (torch.randn(shape, generator=g, device=dev).to(w.torch_dtype) for _ in range(3))
+    out = torch.empty_like(q)
+    frames = sorted({f for c in range(n) for f in w.anchor_frames_for_chunk(c)})
+    a_shape = (max(len(frames), 1) * G, w.heads, w.head_dim)
+    ak, av = (torch.randn(a_shape, generator=g, device=dev).to(w.torch_dtype) for _ in range(2))
+    table = [[frames.index(f) for f in w.anchor_frames_for_chunk(c)] for c in range(n)]
+    flops = sum(4.0 * Nq * (len(table[c]) * G + (c - max(0, c - w.ring_chunks) + 1) * Nq)
+                * w.head_dim * w.heads for c in range(n))
+
+    def launch():
+        ff.packed_attention(q, k, v, n_chunks=n, window=w.ring_chunks, anchor_k=ak, anchor_v=av,
+                            frame_tokens=G, anchors_of_chunk=table, out=out)
+
+    launch()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record(stream)
+    for r in range(reps):
+        launch()
+        ev[r + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = [ev[r].elapsed_time(ev[r + 1]) for r in range(reps)]
+    avg = float(np.mean(ms))
+    tf = flops / (avg * 1e-3) / 1e12
+    log(f"packed clip attention: {n} chunks in one launch, {avg:.2f} ms = {tf:.1f} TFLOP/s")
+    del q, k, v, out, ak, av
+    torch.cuda.empty_cache()
+    return {"chunks": n, "window": w.ring_chunks, "anchor_frames_total": len(frames),
+            "ms_per_launch": round(avg, 3), "tflops": round(tf, 2),
+            "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2)}
+
+
 def copy_calibration() -> int:
     """Three device-to-device copies of 1 GiB (2**28 float32), nothing else."""
     n = 2 ** 28
@@ -203,6 +248,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="14b-720p", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--no-packed", action="store_true",
+                    help="skip the packed whole-clip attention measurement")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     args = ap.parse_args()
@@ -310,6 +357,10 @@ def main() -> int:
                      "traffic_source": traffic_src,
                      "algorithmic_bytes_per_launch": attn_bytes},
     }
+    if not args.no_packed:
+        del ws
+        torch.cuda.empty_cache()
+        result["packed_clip_attention"] = packed_clip(w)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

@@ -16,6 +16,11 @@
  * plus ff_anchor_set, which replaces a layer's anchor segment (the clean
  * anchor KV window A_Gamma(i) of Sec. 3.1).
  *
+ * ff_packed_attention evaluates the same attention for every chunk of one
+ * stage in a single launch (the renderer rows of the packed block-causal
+ * training mask, App. "packed" SFT, Alg. 2), and ff_anchor_partition /
+ * ff_anchor_window compute the planner-side index sets P and Gamma(i).
+ *
  * Conventions shared by every entry point
  * ---------------------------------------
  * Memory.  The caller owns all device memory and all streams.  The cache's
@@ -55,10 +60,11 @@
 extern "C" {
 #endif
 
-#define FF_ABI_VERSION 1
+#define FF_ABI_VERSION 2
 #define FF_MAX_RING_CHUNKS 8     /* W <= 8 */
 #define FF_MAX_ANCHOR_FRAMES 8   /* anchor frames per layer */
 #define FF_MAX_ROPE_FRAMES 16    /* frames per ff_rope3d call */
+#define FF_MAX_PACKED_CHUNKS 128 /* chunks per ff_packed_attention call */
 
 typedef enum {
   FF_OK = 0,
@@ -190,6 +196,96 @@ ff_status ff_cache_anchor_state(const ff_cache* cache, int32_t layer, int32_t* n
  * n_frames*grid_h*grid_w tokens).  k_out / v_out (device) may be NULL. */
 ff_status ff_cache_read(const ff_cache* cache, int32_t stage, int32_t layer, int32_t slot,
                         void* k_out, void* v_out, void* stream);
+
+/* Shape of one packed launch (ff_packed_attention).
+ *   n_chunks          chunks of the clip, 1 .. FF_MAX_PACKED_CHUNKS
+ *   chunk_tokens      tokens per chunk (B_R * grid_h * grid_w)
+ *   num_heads, head_dim (64 or 128), dtype (ff_dtype)
+ *   window            H >= 0: chunk i sees chunks max(0, i - H) .. i
+ *   frame_tokens      tokens per anchor frame (grid_h * grid_w)
+ *   n_anchor_frames   frames held by anchor_k / anchor_v, 0 .. 255
+ *   anchors_of_chunk  host array of n_chunks * FF_MAX_ANCHOR_FRAMES entries:
+ *                     entry [i * FF_MAX_ANCHOR_FRAMES + j] is the index (into
+ *                     the anchor arrays) of an anchor frame chunk i sees, or
+ *                     -1; a frame is listed at most once per chunk, in any
+ *                     order.  May be NULL when n_anchor_frames is 0.        */
+typedef struct {
+  int32_t n_chunks;
+  int32_t chunk_tokens;
+  int32_t num_heads;
+  int32_t head_dim;
+  int32_t window;
+  int32_t frame_tokens;
+  int32_t n_anchor_frames;
+  int32_t dtype;
+  const int32_t* anchors_of_chunk;
+} ff_packed_desc;
+
+/* Packed block-causal attention of one stage over a whole clip (the renderer
+ * rows of the packed training mask M, App. Alg. 2, with the visibility set
+ * Vis(C_i) = chunks max(0, i-H) .. i plus the anchor frames Gamma(i) given
+ * for chunk i).  Per head, the queries of chunk i attend to
+ *   - every token of the anchor frames listed for chunk i,
+ *   - every token of chunks max(0, i - window) .. i (bidirectional in i),
+ * out = softmax(softmax_scale * Q K^T) V.  q, k, v, out are
+ * [n_chunks * chunk_tokens][heads][head_dim] (chunk i's tokens at
+ * i * chunk_tokens); anchor_k / anchor_v are [n_anchor_frames * frame_tokens]
+ * [heads][head_dim] (may be NULL without anchor frames).  Equals
+ * ff_chunk_attention of chunk i after chunks 0 .. i-1 were published into a
+ * ring of W = window (same precision rules).  Tensor pointers must be
+ * 16-byte aligned (FF_ERR_INVALID_ARG).  A run of the read set (one chunk window, or
+ * consecutive anchor frames) may span at most 2^32 - 1 bytes
+ * (FF_ERR_UNSUPPORTED).  Host validation only; one kernel launch. */
+ff_status ff_packed_attention(const ff_packed_desc* desc, const void* q, const void* k,
+                              const void* v, const void* anchor_k, const void* anchor_v,
+                              void* out, float softmax_scale, void* stream);
+
+/* Anchor partition of a clip of L latent frames with anchor spacing delta
+ * (Eq. anchor-infill-partition): P = {m * delta : m * delta < L} u {L - 1},
+ * ascending.  Writes |P| indices to out (host, `capacity` entries) and |P| to
+ * *n_out; FF_ERR_BUFFER if capacity < |P| (*n_out still set).  L >= 1,
+ * delta >= 1.  Host only. */
+ff_status ff_anchor_partition(int32_t L, int32_t delta, int32_t* out, int32_t capacity,
+                              int32_t* n_out);
+
+/* Anchor window Gamma(i) of renderer chunk i (Sec. 3.1): with
+ * u = floor(frames_per_chunk * i / (2 delta)), the frames
+ * {2u delta, (2u+1) delta, (2u+2) delta}, each clamped to L - 1 (near the end
+ * of the clip the boundary anchor L - 1 stands in for anchors past it),
+ * ascending and without repeats.  Writes 1 .. 3 frames to out3 (host) and
+ * their number to *n_out.  i >= 0, frames_per_chunk >= 1, delta >= 1, L >= 1.
+ * Host only. */
+ff_status ff_anchor_window(int64_t i, int32_t frames_per_chunk, int32_t delta, int32_t L,
+                           int32_t* out3, int32_t* n_out);
+
+/* Euler step of the rectified-flow sampler (the Step of the wavefront
+ * algorithm, App. Alg. 1 Phase B): x_out = x - dsigma * v elementwise over n
+ * values of `dtype` (dsigma = sigma_k - sigma_{k-1}).  Each value is
+ * evaluated in float64 as one product and one difference and rounded once to
+ * the dtype (nearest even).  x_out may equal x (in place); the tensors must
+ * not otherwise overlap.  Pointers 16-byte aligned.  n >= 0. */
+ff_status ff_euler_step(const void* x, const void* v, void* x_out, int64_t n, double dsigma,
+                        int32_t dtype, void* stream);
+
+/* Renderer forward of the wavefront: enqueue on `stream` everything rank
+ * `stage` does for chunk `chunk` in one round (obtain x_{i,k} from the
+ * previous stage's hand-off, read, evaluate, Euler step, write; the paper's
+ * k = S - stage).  Returns FF_OK, or a status that stops the run. */
+typedef int32_t (*ff_stage_forward_fn)(void* user, int32_t stage, int64_t chunk, void* stream);
+
+/* Phase B of the wavefront algorithm (App. Alg. 1) on one GPU: stage s runs
+ * on streams[s] as rank s, and in round n = 0 .. n_chunks + n_stages - 2
+ * every rank with 0 <= i = n - s < n_chunks runs forward(user, s, i,
+ * streams[s]).  Rank s's forward of chunk i is ordered after rank s-1's
+ * forward of chunk i (the latent hand-off, through an event) and, by its
+ * stream, after its own forward of chunk i-1 (the ring).  The driver only
+ * enqueues (it creates n_stages events and destroys them when done; HIP keeps
+ * pending waits valid): the caller synchronises the streams.  *n_rounds
+ * receives n_chunks + n_stages - 1 and *n_forwards n_chunks * n_stages (either
+ * may be NULL).  1 <= n_stages <= 64, n_chunks >= 1; streams may repeat. */
+ff_status ff_wavefront_run(int64_t n_chunks, int32_t n_stages, void* const* streams,
+                           ff_stage_forward_fn forward, void* user, int64_t* n_rounds,
+                           int64_t* n_forwards);
 
 /* Name of a status code. */
 const char* ff_status_string(ff_status status);

@@ -337,6 +337,29 @@ def packed_stage_attention(Qs: Sequence[np.ndarray], Ks: Sequence[np.ndarray],
 
 
 # --------------------------------------------------------------------------
+# Sampler step and the wavefront schedule
+# --------------------------------------------------------------------------
+
+def euler_step(x: np.ndarray, v: np.ndarray, dsigma: float, dtype: str) -> np.ndarray:
+    """Euler step of the rectified-flow sampler (wavefront algorithm, Step):
+    x_{k-1} = x_k - (sigma_k - sigma_{k-1}) v, in float64 (product rounded,
+    then the difference), rounded once to the storage dtype ("f64": not rounded)."""
+    x64 = np.asarray(x, np.float64)
+    prod = np.float64(dsigma) * np.asarray(v, np.float64)
+    return x64 - prod if dtype == "f64" else round_to(x64 - prod, dtype)
+
+
+def wavefront_schedule(n_chunks: int, n_stages: int) -> List[List[Tuple[int, int]]]:
+    """Phase B of the wavefront algorithm: round n runs rank r on chunk i = n - r
+    (stage k = S - r) when 0 <= i < N_R; N_R + S - 1 rounds.  Returns, per
+    round, the active (rank, chunk) pairs."""
+    rounds = []
+    for n in range(n_chunks + n_stages - 1):
+        rounds.append([(r, n - r) for r in range(n_stages) if 0 <= n - r < n_chunks])
+    return rounds
+
+
+# --------------------------------------------------------------------------
 # Planner-side index sets and the forward-count model
 # --------------------------------------------------------------------------
 

@@ -128,10 +128,13 @@ struct Cursor {
   int sg, k0;
 };
 
-template <int D>
+// Src is KvSegments (one read set for the whole launch) or PackedPlan (one
+// read set per chunk of a packed clip; q and out then hold every chunk).
+template <int D, class Src>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, int nq, int heads,
-                      float scale_log2, KvSegments segs, int n_qtiles) {
+                      float scale_log2, Src src, int n_qtiles) {
+  constexpr bool kPacked = __is_same(Src, PackedPlan);
   using C = Cfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
   __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
@@ -144,8 +147,15 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   const int xcd = b % kXcds, idx = b / kXcds;
   const int per = n_wg / kXcds, rem = n_wg % kXcds;
   const int logical = xcd * per + min(xcd, rem) + idx;
-  const int head = logical / n_qtiles;
-  const int qt = logical % n_qtiles;
+  int chunk = 0, rest = logical;
+  if constexpr (kPacked) {
+    chunk = logical / (heads * n_qtiles);
+    rest = logical - chunk * (heads * n_qtiles);
+    q += int64_t(chunk) * nq * heads * D;
+    out += int64_t(chunk) * nq * heads * D;
+  }
+  const int head = rest / n_qtiles;
+  const int qt = rest % n_qtiles;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -186,10 +196,15 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   int sg_len = 0;
   uint32_t sg_row_bytes = 0;
   uint64_t sg_k = 0, sg_v = 0;
+  int n_segs;
+  if constexpr (kPacked) n_segs = packed_num_segments(src, chunk);
+  else n_segs = src.n;
 #pragma unroll
   for (int i = 0; i < kMaxSegments; ++i)
-    if (lane == i && i < segs.n) {
-      const KvSegment& sgi = segs.seg[i];
+    if (lane == i && i < n_segs) {
+      KvSegment sgi;
+      if constexpr (kPacked) sgi = packed_segment(src, chunk, i, heads, D, 2);
+      else sgi = src.seg[i];
       sg_len = sgi.len;
       sg_row_bytes = 2u * uint32_t(sgi.tok_stride);
       sg_k = reinterpret_cast<uint64_t>(sgi.k) + 2ull * uint64_t(head) * uint64_t(sgi.head_stride);
@@ -199,7 +214,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
 
   // number of tiles
   int n_tiles = 0;
-  for (int i = 0; i < segs.n; ++i) n_tiles += (seg_len(i) + kBK - 1) / kBK;
+  for (int i = 0; i < n_segs; ++i) n_tiles += (seg_len(i) + kBK - 1) / kBK;
   auto advance = [&](Cursor c) {
     c.k0 += kBK;
     if (c.k0 >= seg_len(c.sg)) {
@@ -453,13 +468,32 @@ hipError_t launch_attention_bf16(const void* q, void* out, int nq, int heads, in
   const dim3 grid(n_qtiles * heads);
   const float scale_log2 = float(double(softmax_scale) * 1.4426950408889634);
   if (head_dim == 128)
-    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(kThreads), 0, stream,
+    hipLaunchKernelGGL((attn_bf16_kernel<128, KvSegments>), grid, dim3(kThreads), 0, stream,
                        static_cast<const __bf16*>(q), static_cast<__bf16*>(out), nq, heads,
                        scale_log2, segs, n_qtiles);
   else
-    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(kThreads), 0, stream,
+    hipLaunchKernelGGL((attn_bf16_kernel<64, KvSegments>), grid, dim3(kThreads), 0, stream,
                        static_cast<const __bf16*>(q), static_cast<__bf16*>(out), nq, heads,
                        scale_log2, segs, n_qtiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_bf16_packed(const void* q, void* out, int heads, int head_dim,
+                                        float softmax_scale, const PackedPlan& plan,
+                                        hipStream_t stream) {
+  const int nq = plan.chunk_tokens;
+  if (nq <= 0 || plan.n_chunks <= 0) return hipSuccess;
+  const int n_qtiles = (nq + kBlockQ - 1) / kBlockQ;
+  const dim3 grid(plan.n_chunks * n_qtiles * heads);
+  const float scale_log2 = float(double(softmax_scale) * 1.4426950408889634);
+  if (head_dim == 128)
+    hipLaunchKernelGGL((attn_bf16_kernel<128, PackedPlan>), grid, dim3(kThreads), 0, stream,
+                       static_cast<const __bf16*>(q), static_cast<__bf16*>(out), nq, heads,
+                       scale_log2, plan, n_qtiles);
+  else
+    hipLaunchKernelGGL((attn_bf16_kernel<64, PackedPlan>), grid, dim3(kThreads), 0, stream,
+                       static_cast<const __bf16*>(q), static_cast<__bf16*>(out), nq, heads,
+                       scale_log2, plan, n_qtiles);
   return hipGetLastError();
 }
 

@@ -2,7 +2,9 @@
 // tiles staged in LDS, online softmax in float32 with expf.  Small sizes
 // only; the bf16 kernel is the fast path.
 //
-// Launch shape: grid (ceil(nq / 128), heads), 128 threads.
+// Launch shape: grid (ceil(nq / 128), heads, chunks), 128 threads; the read
+// set is one KvSegments for the launch or, for a packed clip, the PackedPlan
+// segments of chunk blockIdx.z.
 
 #include <hip/hip_runtime.h>
 
@@ -16,11 +18,14 @@ namespace {
 constexpr int kThreads = 128;
 constexpr int kTileK = 32;
 
-template <int D>
+template <int D, class Src>
 __global__ __launch_bounds__(kThreads) void attn_f32_kernel(const float* __restrict__ q,
                                                             float* __restrict__ out, int nq,
-                                                            int heads, float scale,
-                                                            KvSegments segs) {
+                                                            int heads, float scale, Src src) {
+  constexpr bool kPacked = __is_same(Src, PackedPlan);
+  const int chunk = blockIdx.z;
+  q += int64_t(chunk) * nq * heads * D;
+  out += int64_t(chunk) * nq * heads * D;
   __shared__ float ks[kTileK][D];
   __shared__ float vs[kTileK][D];
   const int head = blockIdx.y;
@@ -36,8 +41,13 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(const float* __restr
   }
   float m = -INFINITY, l = 0.0f;
 
-  for (int sg = 0; sg < segs.n; ++sg) {
-    const KvSegment seg = segs.seg[sg];
+  int n_segs;
+  if constexpr (kPacked) n_segs = packed_num_segments(src, chunk);
+  else n_segs = src.n;
+  for (int sg = 0; sg < n_segs; ++sg) {
+    KvSegment seg;
+    if constexpr (kPacked) seg = packed_segment(src, chunk, sg, heads, D, 4);
+    else seg = src.seg[sg];
     const float* kb = static_cast<const float*>(seg.k) + head * seg.head_stride;
     const float* vb = static_cast<const float*>(seg.v) + head * seg.head_stride;
     for (int k0 = 0; k0 < seg.len; k0 += kTileK) {
@@ -81,15 +91,32 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(const float* __restr
 hipError_t launch_attention_f32(const void* q, void* out, int nq, int heads, int head_dim,
                                 float softmax_scale, const KvSegments& segs, hipStream_t stream) {
   if (nq <= 0) return hipSuccess;
-  dim3 grid((nq + kThreads - 1) / kThreads, heads);
+  dim3 grid((nq + kThreads - 1) / kThreads, heads, 1);
   if (head_dim == 64)
-    hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(kThreads), 0, stream,
+    hipLaunchKernelGGL((attn_f32_kernel<64, KvSegments>), grid, dim3(kThreads), 0, stream,
                        static_cast<const float*>(q), static_cast<float*>(out), nq, heads,
                        softmax_scale, segs);
   else
-    hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(kThreads), 0, stream,
+    hipLaunchKernelGGL((attn_f32_kernel<128, KvSegments>), grid, dim3(kThreads), 0, stream,
                        static_cast<const float*>(q), static_cast<float*>(out), nq, heads,
                        softmax_scale, segs);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_f32_packed(const void* q, void* out, int heads, int head_dim,
+                                       float softmax_scale, const PackedPlan& plan,
+                                       hipStream_t stream) {
+  const int nq = plan.chunk_tokens;
+  if (nq <= 0 || plan.n_chunks <= 0) return hipSuccess;
+  dim3 grid((nq + kThreads - 1) / kThreads, heads, plan.n_chunks);
+  if (head_dim == 64)
+    hipLaunchKernelGGL((attn_f32_kernel<64, PackedPlan>), grid, dim3(kThreads), 0, stream,
+                       static_cast<const float*>(q), static_cast<float*>(out), nq, heads,
+                       softmax_scale, plan);
+  else
+    hipLaunchKernelGGL((attn_f32_kernel<128, PackedPlan>), grid, dim3(kThreads), 0, stream,
+                       static_cast<const float*>(q), static_cast<float*>(out), nq, heads,
+                       softmax_scale, plan);
   return hipGetLastError();
 }
 

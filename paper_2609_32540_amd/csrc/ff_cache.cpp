@@ -10,6 +10,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -390,6 +392,179 @@ ff_status ff_cache_read(const ff_cache* cache, int32_t stage, int32_t layer, int
                                       n_tok, d.num_heads, cache->row_bytes(), head_stride_bytes,
                                       static_cast<hipStream_t>(stream));
   return hip_status(e, "cache_read launch");
+}
+
+ff_status ff_packed_attention(const ff_packed_desc* desc, const void* q, const void* k,
+                              const void* v, const void* anchor_k, const void* anchor_v,
+                              void* out, float softmax_scale, void* stream) {
+  if (!desc) return fail(FF_ERR_INVALID_ARG, "desc is NULL");
+  const ff_packed_desc& d = *desc;
+  if (d.n_chunks < 1 || d.n_chunks > FF_MAX_PACKED_CHUNKS)
+    return fail(FF_ERR_UNSUPPORTED, "n_chunks %d outside [1, %d]", d.n_chunks, FF_MAX_PACKED_CHUNKS);
+  if (d.chunk_tokens < 1 || d.num_heads < 1 || d.window < 0)
+    return fail(FF_ERR_INVALID_ARG, "chunk_tokens and num_heads must be >= 1, window >= 0");
+  if (d.head_dim != 64 && d.head_dim != 128)
+    return fail(FF_ERR_UNSUPPORTED, "head_dim %d (64 or 128 supported)", d.head_dim);
+  if (d.dtype != FF_DT_BF16 && d.dtype != FF_DT_F32)
+    return fail(FF_ERR_UNSUPPORTED, "dtype %d", d.dtype);
+  if (d.n_anchor_frames < 0 || d.n_anchor_frames > 255)
+    return fail(FF_ERR_UNSUPPORTED, "n_anchor_frames %d outside [0, 255]", d.n_anchor_frames);
+  if (d.n_anchor_frames > 0 && (d.frame_tokens < 1 || !d.anchors_of_chunk || !anchor_k || !anchor_v))
+    return fail(FF_ERR_INVALID_ARG,
+                "anchor frames need frame_tokens >= 1, anchors_of_chunk, anchor_k and anchor_v");
+  if (!q || !k || !v || !out) return fail(FF_ERR_INVALID_ARG, "q, k, v and out must be non-NULL");
+  if (check_aligned(q, "q") != FF_OK || check_aligned(k, "k") != FF_OK ||
+      check_aligned(v, "v") != FF_OK || check_aligned(out, "out") != FF_OK)
+    return FF_ERR_INVALID_ARG;
+  if (d.n_anchor_frames > 0 &&
+      (check_aligned(anchor_k, "anchor_k") != FF_OK || check_aligned(anchor_v, "anchor_v") != FF_OK))
+    return FF_ERR_INVALID_ARG;
+  if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
+    return fail(FF_ERR_INVALID_ARG, "softmax_scale must be positive and finite");
+  const int64_t elem = d.dtype == FF_DT_BF16 ? 2 : 4;
+  const int64_t row = elem * d.num_heads * d.head_dim;
+  // the kernels address a run's rows with 32-bit byte offsets
+  const int64_t window_tokens = int64_t(std::min(d.window, d.n_chunks - 1) + 1) * d.chunk_tokens;
+  if (window_tokens * row > int64_t(UINT32_MAX))
+    return fail(FF_ERR_UNSUPPORTED, "a chunk window of %lld tokens spans more than 4 GiB",
+                (long long)window_tokens);
+
+  ff::PackedPlan plan;
+  std::memset(&plan, 0, sizeof(plan));
+  plan.k = k;
+  plan.v = v;
+  plan.ak = anchor_k;
+  plan.av = anchor_v;
+  plan.chunk_tokens = d.chunk_tokens;
+  plan.frame_tokens = d.frame_tokens;
+  plan.window = d.window;
+  plan.n_chunks = d.n_chunks;
+  for (int c = 0; c < d.n_chunks && d.n_anchor_frames > 0; ++c) {
+    bool seen[256] = {false};
+    for (int j = 0; j < FF_MAX_ANCHOR_FRAMES; ++j) {
+      const int32_t f = d.anchors_of_chunk[c * FF_MAX_ANCHOR_FRAMES + j];
+      if (f == -1) continue;
+      if (f < 0 || f >= d.n_anchor_frames)
+        return fail(FF_ERR_RANGE, "chunk %d lists anchor frame %d of %d", c, f, d.n_anchor_frames);
+      if (seen[f]) return fail(FF_ERR_INVALID_ARG, "chunk %d lists anchor frame %d twice", c, f);
+      seen[f] = true;
+    }
+    // runs of consecutive frames, ascending
+    int n_runs = 0;
+    for (int f = 0; f < d.n_anchor_frames;) {
+      if (!seen[f]) { ++f; continue; }
+      int e = f;
+      while (e < d.n_anchor_frames && seen[e]) ++e;
+      if (int64_t(e - f) * d.frame_tokens * row > int64_t(UINT32_MAX))
+        return fail(FF_ERR_UNSUPPORTED, "anchor frames %d .. %d span more than 4 GiB", f, e - 1);
+      plan.runs[c][2 * n_runs] = uint8_t(f);
+      plan.runs[c][2 * n_runs + 1] = uint8_t(e - f);
+      ++n_runs;
+      f = e;
+    }
+  }
+  hipError_t e;
+  if (d.dtype == FF_DT_BF16)
+    e = ff::launch_attention_bf16_packed(q, out, d.num_heads, d.head_dim, softmax_scale, plan,
+                                         static_cast<hipStream_t>(stream));
+  else
+    e = ff::launch_attention_f32_packed(q, out, d.num_heads, d.head_dim, softmax_scale, plan,
+                                        static_cast<hipStream_t>(stream));
+  return hip_status(e, "packed_attention launch");
+}
+
+ff_status ff_anchor_partition(int32_t L, int32_t delta, int32_t* out, int32_t capacity,
+                              int32_t* n_out) {
+  if (L < 1 || delta < 1) return fail(FF_ERR_INVALID_ARG, "L and delta must be >= 1");
+  if (!n_out || (capacity > 0 && !out)) return fail(FF_ERR_INVALID_ARG, "out / n_out is NULL");
+  // {m delta : m delta < L} u {L - 1}; L - 1 is new unless delta divides it
+  const int32_t n_grid = (L - 1) / delta + 1;
+  const int32_t n = n_grid + ((L - 1) % delta != 0 ? 1 : 0);
+  *n_out = n;
+  if (capacity < n) return fail(FF_ERR_BUFFER, "partition has %d entries, capacity %d", n, capacity);
+  for (int32_t m = 0; m < n_grid; ++m) out[m] = m * delta;
+  if (n > n_grid) out[n_grid] = L - 1;
+  return ok();
+}
+
+ff_status ff_anchor_window(int64_t i, int32_t frames_per_chunk, int32_t delta, int32_t L,
+                           int32_t* out3, int32_t* n_out) {
+  if (i < 0 || frames_per_chunk < 1 || delta < 1 || L < 1)
+    return fail(FF_ERR_INVALID_ARG, "need i >= 0, frames_per_chunk >= 1, delta >= 1, L >= 1");
+  if (!out3 || !n_out) return fail(FF_ERR_INVALID_ARG, "out3 / n_out is NULL");
+  const int64_t u = int64_t(frames_per_chunk) * i / (2 * int64_t(delta));
+  int n = 0;
+  for (int64_t m = 2 * u; m <= 2 * u + 2; ++m) {
+    const int64_t f = std::min<int64_t>(m * delta, L - 1);
+    if (n == 0 || out3[n - 1] != f) out3[n++] = int32_t(f);
+  }
+  *n_out = n;
+  return ok();
+}
+
+ff_status ff_euler_step(const void* x, const void* v, void* x_out, int64_t n, double dsigma,
+                        int32_t dtype, void* stream) {
+  if (n < 0) return fail(FF_ERR_INVALID_ARG, "n %lld < 0", (long long)n);
+  if (dtype != FF_DT_BF16 && dtype != FF_DT_F32) return fail(FF_ERR_UNSUPPORTED, "dtype %d", dtype);
+  if (!std::isfinite(dsigma)) return fail(FF_ERR_INVALID_ARG, "dsigma must be finite");
+  if (n == 0) return ok();
+  if (!x || !v || !x_out) return fail(FF_ERR_INVALID_ARG, "x, v and x_out must be non-NULL");
+  if (check_aligned(x, "x") != FF_OK || check_aligned(v, "v") != FF_OK ||
+      check_aligned(x_out, "x_out") != FF_OK)
+    return FF_ERR_INVALID_ARG;
+  const int64_t bytes = n * (dtype == FF_DT_BF16 ? 2 : 4);
+  auto overlap = [&](const void* a, const void* b) {
+    const char* pa = static_cast<const char*>(a);
+    const char* pb = static_cast<const char*>(b);
+    return pa < pb + bytes && pb < pa + bytes;
+  };
+  if (overlap(v, x_out) || (x != x_out && overlap(x, x_out)))
+    return fail(FF_ERR_INVALID_ARG, "x_out overlaps v, or overlaps x without being x");
+  return hip_status(ff::launch_euler(x, v, x_out, n, dsigma, dtype, static_cast<hipStream_t>(stream)),
+                    "euler_step launch");
+}
+
+ff_status ff_wavefront_run(int64_t n_chunks, int32_t n_stages, void* const* streams,
+                           ff_stage_forward_fn forward, void* user, int64_t* n_rounds,
+                           int64_t* n_forwards) {
+  if (n_chunks < 1 || n_stages < 1 || n_stages > 64)
+    return fail(FF_ERR_INVALID_ARG, "need n_chunks >= 1 and 1 <= n_stages <= 64");
+  if (!streams || !forward) return fail(FF_ERR_INVALID_ARG, "streams and forward must be non-NULL");
+  std::vector<hipEvent_t> done(n_stages, nullptr);   // done[s]: rank s's latest forward
+  ff_status st = FF_OK;
+  for (int s = 0; s < n_stages && st == FF_OK; ++s)
+    if (hipEventCreateWithFlags(&done[s], hipEventDisableTiming) != hipSuccess)
+      st = fail(FF_ERR_HIP, "hipEventCreateWithFlags failed");
+  const int64_t rounds = n_chunks + n_stages - 1;
+  int64_t forwards = 0;
+  for (int64_t n = 0; n < rounds && st == FF_OK; ++n) {
+    // ranks in descending order: rank s waits on rank s-1's forward of the same
+    // chunk (round n-1) before rank s-1 records its next one in this round
+    for (int s = n_stages - 1; s >= 0 && st == FF_OK; --s) {
+      const int64_t i = n - s;
+      if (i < 0 || i >= n_chunks) continue;
+      hipStream_t hs = static_cast<hipStream_t>(streams[s]);
+      if (s > 0 && hipStreamWaitEvent(hs, done[s - 1], 0) != hipSuccess) {
+        st = fail(FF_ERR_HIP, "hipStreamWaitEvent failed");
+        break;
+      }
+      const int32_t r = forward(user, s, i, streams[s]);
+      if (r != FF_OK) {
+        st = (r >= 1 && r <= 7) ? ff_status(r) : FF_ERR_INVALID_ARG;
+        if (g_last_error.empty())
+          fail(st, "forward of stage %d, chunk %lld returned %d", s, (long long)i, r);
+        break;
+      }
+      ++forwards;
+      if (hipEventRecord(done[s], hs) != hipSuccess) st = fail(FF_ERR_HIP, "hipEventRecord failed");
+    }
+  }
+  for (hipEvent_t e : done)
+    if (e) (void)hipEventDestroy(e);
+  if (st != FF_OK) return st;
+  if (n_rounds) *n_rounds = rounds;
+  if (n_forwards) *n_forwards = forwards;
+  return ok();
 }
 
 const char* ff_status_string(ff_status status) {

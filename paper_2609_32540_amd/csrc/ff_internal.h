@@ -31,6 +31,51 @@ struct KvSegments {
   int32_t total;  // sum of len
 };
 
+// Read sets of a packed launch (ff_packed_attention): one stage's chunks
+// 0 .. n_chunks-1 in one token-major array, and anchor frames in another.
+// Chunk c reads its anchor frames, grouped into runs of consecutive frames
+// (runs[c] holds (first frame, frame count) pairs; a count of 0 ends the
+// list), then chunks max(0, c - window) .. c as one run of the packed array.
+struct PackedPlan {
+  const void* k;            // [n_chunks * chunk_tokens][heads][d]
+  const void* v;
+  const void* ak;           // [n_frames * frame_tokens][heads][d]
+  const void* av;
+  int32_t chunk_tokens;
+  int32_t frame_tokens;
+  int32_t window;
+  int32_t n_chunks;
+  uint8_t runs[FF_MAX_PACKED_CHUNKS][2 * FF_MAX_ANCHOR_FRAMES];
+};
+
+__host__ __device__ inline int packed_num_segments(const PackedPlan& p, int c) {
+  int n = 0;
+  while (n < FF_MAX_ANCHOR_FRAMES && p.runs[c][2 * n + 1] != 0) ++n;
+  return n + 1;
+}
+
+// Segment i of chunk c's read set, head stride d and token stride heads * d
+// elements (both arrays are token-major).
+__host__ __device__ inline KvSegment packed_segment(const PackedPlan& p, int c, int i, int heads,
+                                                    int d, int elem_bytes) {
+  KvSegment s;
+  s.head_stride = d;
+  s.tok_stride = heads * d;
+  const int64_t row = int64_t(heads) * d * elem_bytes;
+  if (i < packed_num_segments(p, c) - 1) {
+    const int first = p.runs[c][2 * i], count = p.runs[c][2 * i + 1];
+    s.k = static_cast<const char*>(p.ak) + int64_t(first) * p.frame_tokens * row;
+    s.v = static_cast<const char*>(p.av) + int64_t(first) * p.frame_tokens * row;
+    s.len = count * p.frame_tokens;
+  } else {
+    const int c0 = c - p.window > 0 ? c - p.window : 0;
+    s.k = static_cast<const char*>(p.k) + int64_t(c0) * p.chunk_tokens * row;
+    s.v = static_cast<const char*>(p.v) + int64_t(c0) * p.chunk_tokens * row;
+    s.len = (c + 1 - c0) * p.chunk_tokens;
+  }
+  return s;
+}
+
 // Rotation parameters of one ff_rope3d call.
 struct RopeParams {
   double omega[64];                   // frequency of pair p (head_dim / 2 <= 64)
@@ -61,5 +106,19 @@ hipError_t launch_attention_bf16(const void* q, void* out, int nq, int heads, in
 hipError_t launch_attention_f32(const void* q, void* out, int nq, int heads, int head_dim,
                                 float softmax_scale, const KvSegments& segs,
                                 hipStream_t stream);
+
+// Packed launches: q and out are [n_chunks * chunk_tokens][heads][d]; the
+// queries of chunk c read packed_segment(plan, c, .).
+hipError_t launch_attention_bf16_packed(const void* q, void* out, int heads, int head_dim,
+                                        float softmax_scale, const PackedPlan& plan,
+                                        hipStream_t stream);
+
+hipError_t launch_attention_f32_packed(const void* q, void* out, int heads, int head_dim,
+                                       float softmax_scale, const PackedPlan& plan,
+                                       hipStream_t stream);
+
+// Euler step x_out = x - dsigma * v over n elements of dtype (x_out may be x).
+hipError_t launch_euler(const void* x, const void* v, void* y, int64_t n, double dsigma,
+                        int dtype, hipStream_t stream);
 
 }  // namespace ff

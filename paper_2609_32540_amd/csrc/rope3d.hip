@@ -16,6 +16,7 @@
 #include <hip/hip_runtime.h>
 
 #include "ff_internal.h"
+#include "ff_numeric.h"
 
 namespace ff {
 namespace {
@@ -23,35 +24,12 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kTok = 8;
 
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-
-__device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-__device__ inline uint32_t pack_bf16(float a, float b) {
-  f32x2_t f = {a, b};
-  bf16x2_t h = __builtin_convertvector(f, bf16x2_t);  // v_cvt_pk_bf16_f32, nearest even
-  return __builtin_bit_cast(uint32_t, h);
-}
-
-// float64 -> float32 rounded to odd: truncate toward zero and set the last
-// bit when inexact.  Rounding that result to bf16 (8 significant bits, far
-// fewer than float32's 24) to nearest even equals rounding x directly.
-__device__ inline float round_to_odd_f32(double x) {
-  const float r = float(x);  // nearest even
-  const double rd = double(r);
-  if (rd == x) return r;
-  uint32_t bits = __float_as_uint(r);
-  if (fabs(rd) > fabs(x)) bits -= 1;  // one step toward zero
-  return __uint_as_float(bits | 1u);
-}
 
 __device__ inline uint32_t rotate_bf16_pair(uint32_t w, double2 cs) {
   const double a = bf16_lo(w), b = bf16_hi(w);
   const double o0 = a * cs.x - b * cs.y;
   const double o1 = a * cs.y + b * cs.x;
-  return pack_bf16(round_to_odd_f32(o0), round_to_odd_f32(o1));
+  return pack_bf16_rne(round_to_odd_f32(o0), round_to_odd_f32(o1));
 }
 
 template <typename T, int D>

@@ -24,6 +24,8 @@ FF_DT_BF16, FF_DT_F32 = 0, 1
 MAX_RING_CHUNKS = 8
 MAX_ANCHOR_FRAMES = 8
 MAX_ROPE_FRAMES = 16
+MAX_PACKED_CHUNKS = 128
+ABI_VERSION = 2
 
 
 class FFError(RuntimeError):
@@ -47,6 +49,20 @@ class CacheDesc(ctypes.Structure):
     ]
 
 
+class PackedDesc(ctypes.Structure):
+    _fields_ = [
+        ("n_chunks", ctypes.c_int32), ("chunk_tokens", ctypes.c_int32),
+        ("num_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("window", ctypes.c_int32), ("frame_tokens", ctypes.c_int32),
+        ("n_anchor_frames", ctypes.c_int32), ("dtype", ctypes.c_int32),
+        ("anchors_of_chunk", ctypes.POINTER(ctypes.c_int32)),
+    ]
+
+
+# int32_t (*ff_stage_forward_fn)(void* user, int32_t stage, int64_t chunk, void* stream)
+STAGE_FORWARD_FN = ctypes.CFUNCTYPE(ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                    ctypes.c_int64, ctypes.c_void_p)
+
 # (name, restype, argtypes) of every entry point of include/ff.h
 _VP, _I32, _I64, _SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
 _PI32, _PI64 = ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int64)
@@ -62,6 +78,13 @@ SIGNATURES = [
     ("ff_cache_ring_state", _I32, [_VP, _I32, _I32, _PI64, _PI64]),
     ("ff_cache_anchor_state", _I32, [_VP, _I32, _PI32, _PI32]),
     ("ff_cache_read", _I32, [_VP, _I32, _I32, _I32, _VP, _VP, _VP]),
+    ("ff_packed_attention", _I32, [ctypes.POINTER(PackedDesc), _VP, _VP, _VP, _VP, _VP, _VP,
+                                   ctypes.c_float, _VP]),
+    ("ff_anchor_partition", _I32, [_I32, _I32, _PI32, _I32, _PI32]),
+    ("ff_anchor_window", _I32, [_I64, _I32, _I32, _I32, _PI32, _PI32]),
+    ("ff_euler_step", _I32, [_VP, _VP, _VP, _I64, ctypes.c_double, _I32, _VP]),
+    ("ff_wavefront_run", _I32, [_I64, _I32, ctypes.POINTER(_VP), STAGE_FORWARD_FN, _VP, _PI64,
+                                _PI64]),
     ("ff_status_string", ctypes.c_char_p, [_I32]),
     ("ff_last_error", ctypes.c_char_p, []),
 ]
@@ -225,3 +248,133 @@ class RendererCache:
             _check(lib().ff_cache_read(self._h, stage, layer, slot, k.data_ptr(), v.data_ptr(),
                                        _stream_handle(self.device, stream)))
         return k, v
+
+
+# ----------------------------------------------------------------------
+def _dense(t: torch.Tensor, shape: Tuple[int, ...], dtype: torch.dtype, device: torch.device,
+           name: str) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device != device or t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} on {device} (got {t.dtype} on {t.device})")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def packed_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, *, n_chunks: int,
+                     window: int, anchor_k: Optional[torch.Tensor] = None,
+                     anchor_v: Optional[torch.Tensor] = None, frame_tokens: int = 0,
+                     anchors_of_chunk: Optional[Sequence[Sequence[int]]] = None,
+                     out: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+                     stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """ff_packed_attention: every chunk of one stage in one launch.
+
+    q, k, v: [n_chunks * chunk_tokens][heads][d]; anchor_k / anchor_v:
+    [n_frames * frame_tokens][heads][d]; anchors_of_chunk[i] lists the anchor
+    frame indices chunk i sees.
+    """
+    if q.dim() != 3 or q.shape[0] % n_chunks:
+        raise ValueError("q must be [n_chunks * chunk_tokens][heads][d]")
+    chunk_tokens = q.shape[0] // n_chunks
+    heads, d = q.shape[1], q.shape[2]
+    dev, dt = q.device, q.dtype
+    if dt not in (torch.bfloat16, torch.float32):
+        raise ValueError("dtype must be torch.bfloat16 or torch.float32")
+    shape = (n_chunks * chunk_tokens, heads, d)
+    qp = _dense(q, shape, dt, dev, "q")
+    kp = _dense(k, shape, dt, dev, "k")
+    vp = _dense(v, shape, dt, dev, "v")
+    if out is None:
+        out = torch.empty_like(q)
+    op = _dense(out, shape, dt, dev, "out")
+    n_frames = 0
+    akp = avp = None
+    table = None
+    if anchor_k is not None:
+        if frame_tokens < 1 or anchor_k.shape[0] % frame_tokens:
+            raise ValueError("anchor_k must hold whole frames of frame_tokens tokens")
+        n_frames = anchor_k.shape[0] // frame_tokens
+        a_shape = (n_frames * frame_tokens, heads, d)
+        akp = _dense(anchor_k, a_shape, dt, dev, "anchor_k")
+        avp = _dense(anchor_v, a_shape, dt, dev, "anchor_v")
+        flat = [-1] * (n_chunks * MAX_ANCHOR_FRAMES)
+        for i, frames in enumerate(anchors_of_chunk or []):
+            if len(frames) > MAX_ANCHOR_FRAMES:
+                raise ValueError(f"chunk {i} lists more than {MAX_ANCHOR_FRAMES} anchor frames")
+            for j, f in enumerate(frames):
+                flat[i * MAX_ANCHOR_FRAMES + j] = int(f)
+        table = (ctypes.c_int32 * len(flat))(*flat)
+    desc = PackedDesc(n_chunks, chunk_tokens, heads, d, window, frame_tokens, n_frames,
+                      FF_DT_BF16 if dt == torch.bfloat16 else FF_DT_F32,
+                      ctypes.cast(table, ctypes.POINTER(ctypes.c_int32)) if table is not None else None)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _check(lib().ff_packed_attention(ctypes.byref(desc), qp, kp, vp, akp, avp, op,
+                                     ctypes.c_float(scale), _stream_handle(dev, stream)))
+    return out
+
+
+def anchor_partition(L: int, delta: int) -> List[int]:
+    """ff_anchor_partition: P = {m delta < L} u {L - 1}."""
+    n = ctypes.c_int32()
+    lib().ff_anchor_partition(L, delta, None, 0, ctypes.byref(n))   # size query
+    if n.value <= 0:
+        _check(lib().ff_anchor_partition(L, delta, None, 0, ctypes.byref(n)))
+    buf = (ctypes.c_int32 * n.value)()
+    _check(lib().ff_anchor_partition(L, delta, buf, n.value, ctypes.byref(n)))
+    return list(buf)
+
+
+def anchor_window(i: int, frames_per_chunk: int, delta: int, L: int) -> List[int]:
+    """ff_anchor_window: Gamma(i)."""
+    out = (ctypes.c_int32 * 3)()
+    n = ctypes.c_int32()
+    _check(lib().ff_anchor_window(i, frames_per_chunk, delta, L, out, ctypes.byref(n)))
+    return list(out)[: n.value]
+
+
+def euler_step(x: torch.Tensor, v: torch.Tensor, dsigma: float, out: Optional[torch.Tensor] = None,
+               stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """ff_euler_step: out = x - dsigma * v (out may be x)."""
+    if x.dtype not in (torch.bfloat16, torch.float32) or v.dtype != x.dtype:
+        raise ValueError("x and v must both be bf16 or both float32")
+    if x.shape != v.shape or not x.is_contiguous() or not v.is_contiguous():
+        raise ValueError("x and v must be contiguous tensors of one shape")
+    if out is None:
+        out = torch.empty_like(x)
+    if out.shape != x.shape or out.dtype != x.dtype or not out.is_contiguous():
+        raise ValueError("out must match x")
+    _check(lib().ff_euler_step(x.data_ptr(), v.data_ptr(), out.data_ptr(), x.numel(),
+                               ctypes.c_double(dsigma),
+                               FF_DT_BF16 if x.dtype == torch.bfloat16 else FF_DT_F32,
+                               _stream_handle(x.device, stream)))
+    return out
+
+
+def wavefront_run(n_chunks: int, streams: Sequence[torch.cuda.Stream], forward) -> Tuple[int, int]:
+    """ff_wavefront_run: rank s = stage s on streams[s]; forward(stage, chunk, stream) enqueues
+    one renderer forward on `stream` (a torch stream) and returns nothing.  Returns
+    (rounds, forwards).  The caller synchronises the streams."""
+    by_handle = {s.cuda_stream: s for s in streams}
+    errors = []
+
+    def cb(_user, stage, chunk, handle):
+        try:
+            forward(int(stage), int(chunk), by_handle[handle or 0])
+            return FF_OK
+        except Exception as e:  # stop the run, report after it returns
+            errors.append(e)
+            return 1
+
+    fn = STAGE_FORWARD_FN(cb)
+    arr = (ctypes.c_void_p * len(streams))(*[s.cuda_stream for s in streams])
+    rounds, forwards = ctypes.c_int64(), ctypes.c_int64()
+    st = lib().ff_wavefront_run(n_chunks, len(streams), arr, fn, None, ctypes.byref(rounds),
+                                ctypes.byref(forwards))
+    if errors:
+        raise errors[0]
+    _check(st)
+    return rounds.value, forwards.value

@@ -34,11 +34,11 @@ def desc(**kw):
 def test_library_exports_every_header_symbol():
     L = ff.lib()
     names = header_functions()
-    assert len(names) == 13
+    assert len(names) == 18
     for n in names:
         assert hasattr(L, n), n
     assert {n for n, _, _ in ff.SIGNATURES} == set(names)
-    assert L.ff_abi_version() == 1
+    assert L.ff_abi_version() == ff.ABI_VERSION == 2
 
 
 def test_cache_bytes_layout():
@@ -132,3 +132,102 @@ def test_status_strings():
     L = ff.lib()
     for code, name in ff.STATUS_NAMES.items():
         assert L.ff_status_string(code).decode() == name
+
+
+# ----------------------------------------------------------------------
+# ff_packed_attention: host validation (every case fails before a launch)
+
+def packed_desc(**kw):
+    base = dict(n_chunks=6, chunk_tokens=192, num_heads=2, head_dim=64, window=2, frame_tokens=64,
+                n_anchor_frames=0, dtype=ff.FF_DT_BF16, anchors_of_chunk=None)
+    base.update(kw)
+    return ff.PackedDesc(**base)
+
+
+def packed_call(d, q=FAKE_DEV, k=FAKE_DEV, v=FAKE_DEV, ak=None, av=None, out=FAKE_DEV, scale=0.125):
+    L = ff.lib()
+    return L.ff_packed_attention(ctypes.byref(d) if d is not None else None, q, k, v, ak, av, out,
+                                 ctypes.c_float(scale), None)
+
+
+def table(rows):
+    flat = [-1] * (len(rows) * ff.MAX_ANCHOR_FRAMES)
+    for i, r in enumerate(rows):
+        for j, f in enumerate(r):
+            flat[i * ff.MAX_ANCHOR_FRAMES + j] = f
+    arr = (ctypes.c_int32 * len(flat))(*flat)
+    return arr, ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_chunks=0), 5), (dict(n_chunks=129), 5), (dict(chunk_tokens=0), 1),
+    (dict(num_heads=0), 1), (dict(window=-1), 1), (dict(head_dim=96), 5), (dict(dtype=3), 5),
+    (dict(n_anchor_frames=256), 5), (dict(n_anchor_frames=2), 1),   # no table / pointers
+])
+def test_packed_desc_rejected(kw, status):
+    assert packed_call(packed_desc(**kw)) == status
+    assert ff.lib().ff_last_error().decode()
+
+
+def test_packed_pointer_and_table_validation():
+    assert packed_call(None) == 1
+    assert packed_call(packed_desc(), q=None) == 1
+    assert packed_call(packed_desc(), out=FAKE_DEV + 8) == 1          # misaligned
+    assert packed_call(packed_desc(), scale=0.0) == 1
+    arr, ptr = table([[0, 1]] * 6)
+    ok_anchor = dict(n_anchor_frames=2, anchors_of_chunk=ptr)
+    assert packed_call(packed_desc(**ok_anchor), ak=FAKE_DEV, av=FAKE_DEV + 8) == 1
+    arr2, ptr2 = table([[0, 1]] * 5 + [[1, 1]])                       # a frame listed twice
+    assert packed_call(packed_desc(n_anchor_frames=2, anchors_of_chunk=ptr2), ak=FAKE_DEV,
+                       av=FAKE_DEV) == 1
+    arr3, ptr3 = table([[0, 2]] * 6)                                  # frame 2 of 2
+    assert packed_call(packed_desc(n_anchor_frames=2, anchors_of_chunk=ptr3), ak=FAKE_DEV,
+                       av=FAKE_DEV) == 4
+    # a chunk window wider than 4 GiB of bytes
+    big = packed_desc(n_chunks=8, chunk_tokens=1 << 20, num_heads=40, head_dim=128, window=4)
+    assert packed_call(big) == 5
+
+
+# ----------------------------------------------------------------------
+# planner-side index sets: the C helpers against the oracle
+
+def test_anchor_partition_matches_oracle():
+    from oracle import ff_oracle as fo
+    for L in list(range(1, 70)) + [81, 161, 261, 321]:
+        for delta in (1, 2, 3, 7, 10, 24):
+            assert ff.anchor_partition(L, delta) == fo.anchor_partition(L, delta), (L, delta)
+    n = ctypes.c_int32()
+    buf = (ctypes.c_int32 * 2)()
+    assert ff.lib().ff_anchor_partition(261, 10, buf, 2, ctypes.byref(n)) == 7  # too small
+    assert n.value == 27
+    assert ff.lib().ff_anchor_partition(0, 10, buf, 2, ctypes.byref(n)) == 1
+
+
+def test_anchor_window_matches_oracle():
+    from oracle import ff_oracle as fo
+    for L in (18, 21, 81, 261):
+        for B_R in (1, 3, 4):
+            for delta in (5, 10):
+                for i in range(0, -(-L // B_R) + 3):
+                    assert ff.anchor_window(i, B_R, delta, L) == fo.anchor_window(i, B_R, delta, L)
+    out = (ctypes.c_int32 * 3)()
+    n = ctypes.c_int32()
+    assert ff.lib().ff_anchor_window(-1, 3, 10, 261, out, ctypes.byref(n)) == 1
+
+
+def test_euler_and_wavefront_host_validation():
+    L = ff.lib()
+    assert L.ff_euler_step(FAKE_DEV, FAKE_DEV + 4096, FAKE_DEV, -1, 0.5, 0, None) == 1
+    assert L.ff_euler_step(FAKE_DEV, FAKE_DEV + 4096, FAKE_DEV, 8, 0.5, 9, None) == 5
+    assert L.ff_euler_step(FAKE_DEV, FAKE_DEV + 4096, FAKE_DEV, 8, float("nan"), 0, None) == 1
+    assert L.ff_euler_step(FAKE_DEV, FAKE_DEV + 8, FAKE_DEV + 4096, 8, 0.5, 0, None) == 1  # misaligned v
+    assert L.ff_euler_step(FAKE_DEV, FAKE_DEV + 4096, FAKE_DEV + 4096 + 16, 64, 0.5, 0, None) == 1  # out overlaps v
+    assert L.ff_euler_step(FAKE_DEV, FAKE_DEV + 4096, FAKE_DEV + 16, 64, 0.5, 0, None) == 1  # out overlaps x
+    assert L.ff_euler_step(None, None, None, 0, 0.5, 0, None) == 0                          # empty
+    calls = []
+    fn = ff.STAGE_FORWARD_FN(lambda u, s, c, st: calls.append((s, c)) or 0)
+    arr = (ctypes.c_void_p * 2)(None, None)
+    r, f = ctypes.c_int64(), ctypes.c_int64()
+    assert L.ff_wavefront_run(0, 2, arr, fn, None, ctypes.byref(r), ctypes.byref(f)) == 1
+    assert L.ff_wavefront_run(3, 0, arr, fn, None, ctypes.byref(r), ctypes.byref(f)) == 1
+    assert not calls

@@ -1,0 +1,170 @@
+"""GPU parity of ff_packed_attention (every chunk of one stage in one launch,
+the renderer rows of the packed block-causal training mask) against the
+oracle's packed mask, and against the sequential ring path on the same
+inputs.  Bars as in test_gpu_parity: bf16 within max-abs 2e-2 and relative-L2
+5e-3 of float64, float32 within 1e-5."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import ff_oracle as fo
+from paper_2609_32540_amd import ff
+
+from gpu_util import check_attention, exact, make_cache, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _needs_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ff.lib()
+
+
+def clip(w, n_chunks, stage=0, layer=0):
+    """Packed Q, K, V of chunks 0 .. n_chunks-1 at (stage, layer)."""
+    parts = [[synth.chunk_tensor(w, t, c, stage, layer) for c in range(n_chunks)]
+             for t in (synth.T_Q, synth.T_K, synth.T_V)]
+    return [torch.cat(p, 0) for p in parts]
+
+
+def oracle_packed(w, q, k, v, ak, av, table, window, scale):
+    Nq, G = w.chunk_tokens, w.tokens_per_frame
+    n = q.shape[0] // Nq
+    Qs = [exact(q[c * Nq:(c + 1) * Nq]) for c in range(n)]
+    Ks = [exact(k[c * Nq:(c + 1) * Nq]) for c in range(n)]
+    Vs = [exact(v[c * Nq:(c + 1) * Nq]) for c in range(n)]
+    frames = {}
+    if ak is not None:
+        for f in range(ak.shape[0] // G):
+            frames[f] = (exact(ak[f * G:(f + 1) * G]), exact(av[f * G:(f + 1) * G]))
+    return fo.packed_stage_attention(Qs, Ks, Vs, frames, table if ak is not None else [[]] * n,
+                                     window, scale)
+
+
+def run_and_check(w, n_chunks, window, table, n_frames):
+    q, k, v = (to_dev(t) for t in clip(w, n_chunks))
+    ak = av = None
+    if n_frames:
+        a_k, a_v = synth.anchor_tensors(w, list(range(n_frames)), 0)
+        ak, av = to_dev(a_k), to_dev(a_v)
+    scale = 1.0 / math.sqrt(w.head_dim)
+    out = ff.packed_attention(q, k, v, n_chunks=n_chunks, window=window, anchor_k=ak, anchor_v=av,
+                              frame_tokens=w.tokens_per_frame, anchors_of_chunk=table, scale=scale)
+    torch.cuda.synchronize()
+    ref = oracle_packed(w, q, k, v, ak, av, table, window, scale)
+    Nq = w.chunk_tokens
+    got = exact(out)
+    for c in range(n_chunks):
+        check_attention(got[c * Nq:(c + 1) * Nq], ref[c], w.dtype, f"chunk {c}")
+    return out
+
+
+def small(dtype, head_dim, grid=(6, 11), **kw):
+    base = dict(dtype=dtype, heads=2, head_dim=head_dim, grid_h=grid[0], grid_w=grid[1],
+                ring_chunks=2, stages=1, layers=1, n_chunks=6, anchor_rule="none",
+                max_anchor_frames=3)
+    base.update(kw)
+    return synth.small_workload("packed", **base)
+
+
+# anchor tables with unsorted entries, gaps (several runs), empty rows and a full row
+TABLE6 = [[], [2, 0], [0, 1, 2], [1], [2, 1], [0, 2]]
+
+
+@pytest.mark.parametrize("dtype,d,grid", [("f32", 64, (8, 8)), ("bf16", 64, (6, 11)),
+                                          ("bf16", 128, (6, 11)), ("bf16", 128, (10, 20))])
+@pytest.mark.parametrize("window", [0, 1, 2, 9])
+def test_packed_matches_oracle(dtype, d, grid, window):
+    w = small(dtype, d, grid)
+    run_and_check(w, 6, window, TABLE6, 3)
+
+
+def test_packed_without_anchors_tiny_workload():
+    w = synth.WORKLOADS["tiny-f32"]
+    run_and_check(w, w.n_chunks, w.ring_chunks, None, 0)
+
+
+def test_packed_single_chunk_and_short_chunks():
+    # one chunk (only its own keys), and 1-frame chunks of 18 tokens (a single partial tile)
+    w = small("bf16", 128)
+    run_and_check(w, 1, 3, [[0]], 1)
+    w2 = small("bf16", 64, grid=(3, 6), frames_per_chunk=1)
+    run_and_check(w2, 5, 2, [[0], [], [0], [0], []], 1)
+
+
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
+def test_packed_equals_sequential_ring(dtype, d):
+    """Chunk i of the packed launch against ff_chunk_attention of chunk i after
+    chunks 0 .. i-1 were published into a ring of W = window, anchors set to
+    chunk i's frames: both within the bar of the oracle, and (f32) equal to
+    each other within 1e-5."""
+    w = small(dtype, d, grid=(6, 11), ring_chunks=2)
+    n, W = 6, 2
+    q, k, v = (to_dev(t) for t in clip(w, n))
+    a_k, a_v = synth.anchor_tensors(w, [0, 1, 2], 0)
+    ak, av = to_dev(a_k), to_dev(a_v)
+    scale = 1.0 / math.sqrt(d)
+    packed = ff.packed_attention(q, k, v, n_chunks=n, window=W, anchor_k=ak, anchor_v=av,
+                                 frame_tokens=w.tokens_per_frame, anchors_of_chunk=TABLE6,
+                                 scale=scale)
+    cache = make_cache(w, stages=1, layers=1)
+    Nq, G = w.chunk_tokens, w.tokens_per_frame
+    seq = torch.empty_like(q)
+    for c in range(n):
+        fr = TABLE6[c]
+        if fr:
+            kk = torch.cat([ak[f * G:(f + 1) * G] for f in fr])
+            vv = torch.cat([av[f * G:(f + 1) * G] for f in fr])
+            cache.anchor_set(0, fr, kk.contiguous(), vv.contiguous())
+        else:
+            cache.anchor_set(0, [], None, None)
+        sl = slice(c * Nq, (c + 1) * Nq)
+        cache.chunk_attention(0, 0, c, q[sl], k[sl], v[sl], seq[sl], scale=scale)
+        cache.kv_publish(0, 0, c, k[sl], v[sl])
+    torch.cuda.synchronize()
+    ref = oracle_packed(w, q, k, v, ak, av, TABLE6, W, scale)
+    gp, gs = exact(packed), exact(seq)
+    for c in range(n):
+        sl = slice(c * Nq, (c + 1) * Nq)
+        check_attention(gp[sl], ref[c], dtype, f"packed chunk {c}")
+        check_attention(gs[sl], ref[c], dtype, f"sequential chunk {c}")
+    if dtype == "f32":
+        assert np.abs(gp - gs).max() <= 1e-5
+
+
+def test_packed_full_size_sampled_rows():
+    """1.3B 480p clip (27 chunks x 4680 tokens, 12 heads x 128, W = 4, anchor
+    windows Gamma(i)): one launch, checked on sampled rows of chunks at the
+    start, the middle and the end against the float64 oracle over the visible
+    keys; inputs seeded N(0,1) drawn on the device."""
+    w = synth.WORKLOADS["1.3b-480p"]
+    n, W, Nq, G = w.n_chunks, w.ring_chunks, w.chunk_tokens, w.tokens_per_frame
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(1234)
+    shape = (n * Nq, w.heads, w.head_dim)
+    q, k, v = (torch.randn(shape, generator=g, device=dev).to(torch.bfloat16) for _ in range(3))
+    frames = sorted({f for c in range(n) for f in w.anchor_frames_for_chunk(c)})
+    a_shape = (len(frames) * G, w.heads, w.head_dim)
+    ak, av = (torch.randn(a_shape, generator=g, device=dev).to(torch.bfloat16) for _ in range(2))
+    table = [[frames.index(f) for f in w.anchor_frames_for_chunk(c)] for c in range(n)]
+    scale = 1.0 / math.sqrt(w.head_dim)
+    out = ff.packed_attention(q, k, v, n_chunks=n, window=W, anchor_k=ak, anchor_v=av,
+                              frame_tokens=G, anchors_of_chunk=table, scale=scale)
+    torch.cuda.synchronize()
+    rows = np.concatenate([np.arange(0, 256), np.arange(Nq - 200, Nq)])
+    for c in (0, 3, 13, n - 1):
+        keys = [slice(f * G, (f + 1) * G) for f in table[c]]
+        chunks = slice(max(0, c - W) * Nq, (c + 1) * Nq)
+        for h in (0, w.heads - 1):
+            Kh = np.concatenate([exact(ak[s, h]) for s in keys] + [exact(k[chunks, h])])
+            Vh = np.concatenate([exact(av[s, h]) for s in keys] + [exact(v[chunks, h])])
+            Qh = exact(q[c * Nq + rows, h])
+            ref = fo.attend(Qh.astype(np.float64), Kh.astype(np.float64), Vh.astype(np.float64),
+                            scale)
+            check_attention(exact(out[c * Nq + rows, h]), ref, "bf16", f"chunk {c} head {h}")

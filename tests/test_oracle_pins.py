@@ -408,3 +408,49 @@ def test_video_lengths_map_to_chunks():
     for s, L in zip(ex["seconds"], ex["latents"]):
         assert 1 + 4 * (L - 1) == 16 * s + 1
         assert fo.num_blocks(L, 3) * 3 == L
+
+
+# --------------------------------------------------------------------------
+# Euler step and wavefront schedule
+
+def test_euler_step_follows_rectified_flow_path():
+    """On the linear path x_s = (1 - s) x0 + s eps with its exact velocity
+    v = eps - x0, one Euler step from sigma_k lands on x at sigma_{k-1}."""
+    rng = np.random.default_rng(3)
+    x0, eps = rng.standard_normal((2, 4096))
+    sig = [1.0, 0.75, 0.5, 0.25, 0.0]
+    x = eps.copy()
+    for k in range(4):
+        x = fo.euler_step(x, eps - x0, sig[k] - sig[k + 1], "f64")
+        np.testing.assert_allclose(x, (1 - sig[k + 1]) * x0 + sig[k + 1] * eps, atol=1e-14)
+    np.testing.assert_allclose(x, x0, atol=1e-14)
+
+
+def test_euler_step_rounds_once_to_storage():
+    x = np.array([1.0, 1.0, -3.0, 0.0])
+    v = np.array([2.0 ** -9, 2.0 ** -8, 0.5, 7.0])
+    got = fo.euler_step(x, v, -1.0, "bf16")            # x + v
+    # bf16 spacing at 1 is 2^-7: 1 + 2^-9 rounds down, 1 + 2^-8 is the tie and goes to the
+    # even neighbour 1; -3 + 0.5 and 0 + 7 are exact
+    np.testing.assert_array_equal(got, [1.0, 1.0, -2.5, 7.0])
+    assert fo.euler_step(np.array([5.0]), np.array([123.0]), 0.0, "bf16")[0] == 5.0
+
+
+@pytest.mark.parametrize("N_R,S", [(1, 1), (6, 4), (27, 4), (3, 5)])
+def test_wavefront_schedule_rounds_and_coverage(N_R, S):
+    rounds = fo.wavefront_schedule(N_R, S)
+    assert len(rounds) == N_R + S - 1
+    items = [it for r in rounds for it in r]
+    assert sorted(items) == sorted((r, i) for r in range(S) for i in range(N_R))  # N_R S forwards
+    pos = {it: n for n, r in enumerate(rounds) for it in r}
+    for r in range(S):
+        for i in range(N_R):
+            if r > 0:
+                assert pos[(r, i)] == pos[(r - 1, i)] + 1     # the hand-off of x_{i,k}
+            if i > 0:
+                assert pos[(r, i)] == pos[(r, i - 1)] + 1     # the stage's ring, chunk order
+    # the renderer share of the forward-count model is N_R * S
+    L, B = 3 * N_R, 3
+    total, _, _ = fo.forward_counts(L, 10, B, S)
+    M = len(fo.anchor_partition(L, 10))
+    assert total - fo.num_blocks(M, B) * (S + 1) == N_R * S
