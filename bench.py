@@ -192,6 +192,76 @@ def packed_clip(w: synth.Workload, reps: int = 3) -> dict:
             "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2)}
 
 
+def wavefront_clip(name: str = "1.3b-480p") -> dict:
+    """One-GPU wavefront (one HIP stream per stage) against chunk-major order
+    on one stream, over a whole clip of one layer of the workload.
+
+    The forward of (stage, chunk) is a stub around the hot path: Q/K/V from
+    the chunk's latent (elementwise), 3D RoPE, attention over [Gamma(i) from
+    the anchor bank | the stage's ring | the chunk], publish, and the Euler
+    step that hands the latent to the next stage.  Wall time of the whole
+    clip, inputs resident in HBM, seeded N(0,1) on the device.
+    """
+    w = synth.WORKLOADS[name]
+    dev = torch.device("cuda", 0)
+    S, N_R, G = w.stages, w.n_chunks, w.tokens_per_frame
+    sig = [1.0 - j / S for j in range(S, -1, -1)]   # sigma_0 = 0 .. sigma_S = 1
+    frames = sorted({f for i in range(N_R) for f in w.anchor_frames_for_chunk(i)})
+    g = torch.Generator(device=dev)
+    g.manual_seed(3)
+    bank_k = torch.randn((len(frames) * G, w.heads, w.head_dim), generator=g, device=dev).to(w.torch_dtype)
+    bank_v = torch.randn_like(bank_k, dtype=torch.float32).to(w.torch_dtype)
+    noise = [torch.randn((w.chunk_tokens, w.heads, w.head_dim), generator=g, device=dev)
+             .to(w.torch_dtype) for _ in range(N_R)]
+    windows = [[frames.index(f) for f in w.anchor_frames_for_chunk(i)] for i in range(N_R)]
+
+    def run(streams):
+        cache = ff.RendererCache(stages=S, layers=1, ring_chunks=w.ring_chunks,
+                                 frames_per_chunk=w.frames_per_chunk, grid_h=w.grid_h,
+                                 grid_w=w.grid_w, heads=w.heads, head_dim=w.head_dim,
+                                 max_anchor_frames=1, dtype=w.torch_dtype, device=dev)
+        X = [t.clone() for t in noise]
+        torch.cuda.synchronize()
+
+        def forward(s, i, stream):
+            with torch.cuda.stream(stream):
+                x = X[i]
+                q, k, v = x.clone(), (x * 0.5).to(x.dtype), (x + 0.25).to(x.dtype)
+                cache.rope3d(q, k, [w.frames_per_chunk * i + f for f in range(w.frames_per_chunk)],
+                             stream=stream)
+                h = cache.chunk_attention_bank(s, 0, i, q, k, v, bank_k, bank_v, windows[i],
+                                               stream=stream)
+                cache.kv_publish(s, 0, i, k, v, stream=stream)
+                kk = S - s
+                ff.euler_step(x, h, sig[kk] - sig[kk - 1], out=x, stream=stream)
+
+        t0 = time.perf_counter()
+        if len(streams) == 1:
+            for i in range(N_R):
+                for s in range(S):
+                    forward(s, i, streams[0])
+            rounds, fwd = N_R + S - 1, N_R * S
+        else:
+            rounds, fwd = ff.wavefront_run(N_R, streams, forward)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        del cache
+        return el, rounds, fwd, X
+
+    one = [torch.cuda.Stream()]
+    many = [torch.cuda.Stream() for _ in range(S)]
+    run(one)                                   # warm (allocator, code objects)
+    t_seq, _, _, X_seq = run(one)
+    t_wave, rounds, fwd, X_wave = run(many)
+    same = all(torch.equal(a, b) for a, b in zip(X_seq, X_wave))
+    log(f"wavefront {name}: {rounds} rounds, {fwd} forwards, {t_wave * 1e3:.1f} ms on {S} streams "
+        f"vs {t_seq * 1e3:.1f} ms chunk-major on one stream; identical latents: {same}")
+    return {"workload": name, "layers": 1, "stages": S, "chunks": N_R, "rounds": rounds,
+            "forwards": fwd, "ms_wavefront_streams": round(t_wave * 1e3, 2),
+            "ms_chunk_major_one_stream": round(t_seq * 1e3, 2),
+            "speedup": round(t_seq / t_wave, 3), "latents_identical": bool(same)}
+
+
 def copy_calibration() -> int:
     """Three device-to-device copies of 1 GiB (2**28 float32), nothing else."""
     n = 2 ** 28
@@ -250,6 +320,8 @@ def main() -> int:
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--no-packed", action="store_true",
                     help="skip the packed whole-clip attention measurement")
+    ap.add_argument("--no-wavefront", action="store_true",
+                    help="skip the one-GPU wavefront measurement")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     args = ap.parse_args()
@@ -357,10 +429,12 @@ def main() -> int:
                      "traffic_source": traffic_src,
                      "algorithmic_bytes_per_launch": attn_bytes},
     }
+    del ws
+    torch.cuda.empty_cache()
     if not args.no_packed:
-        del ws
-        torch.cuda.empty_cache()
         result["packed_clip_attention"] = packed_clip(w)
+    if not args.no_wavefront:
+        result["wavefront_clip"] = wavefront_clip()
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

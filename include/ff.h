@@ -179,6 +179,23 @@ ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int6
                              const void* q, const void* k_cur, const void* v_cur, void* out,
                              float softmax_scale, void* stream);
 
+/* ff_chunk_attention with the anchor KV read from a caller-owned anchor bank
+ * instead of the layer's anchor segment (the bank A of Sec. 3.1 / App. Alg. 1,
+ * here in device memory): the anchors visible to the chunk are the n_frames
+ * frames bank[frame_index[j]] (host array of distinct indices, in any order,
+ * 0 <= n_frames <= FF_MAX_ANCHOR_FRAMES), where bank_k / bank_v are
+ * token-major [bank_frames * grid_h * grid_w][heads][head_dim] arrays of the
+ * cache dtype (K already rotated).  The layer's anchor segment is not read,
+ * so different stages may read different windows at the same time (the
+ * wavefront runs chunks i, i-1, .. on its stages together).  Everything else
+ * as ff_chunk_attention.  A run of consecutive bank frames may span at most
+ * 2^32 - 1 bytes (FF_ERR_UNSUPPORTED). */
+ff_status ff_chunk_attention_bank(ff_cache* cache, int32_t stage, int32_t layer,
+                                  int64_t chunk_index, const void* q, const void* k_cur,
+                                  const void* v_cur, void* out, float softmax_scale,
+                                  const void* bank_k, const void* bank_v, int32_t n_frames,
+                                  const int32_t* frame_index, void* stream);
+
 /* Host bookkeeping of one ring: slot_chunk[s] (W entries, host) is the chunk
  * held by slot s or -1; *published_count is the next chunk the ring expects
  * (0 if nothing was published).  Either output may be NULL. */

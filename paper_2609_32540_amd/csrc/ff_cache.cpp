@@ -271,9 +271,14 @@ ff_status ff_anchor_set(ff_cache* cache, int32_t layer, int32_t n_frames, const 
   return ok();
 }
 
-ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
-                             const void* q, const void* k_cur, const void* v_cur, void* out,
-                             float softmax_scale, void* stream) {
+namespace {
+
+// Shared body of ff_chunk_attention and ff_chunk_attention_bank.  bank_k ==
+// nullptr selects the layer's anchor segment.
+ff_status chunk_attention_impl(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
+                               const void* q, const void* k_cur, const void* v_cur, void* out,
+                               float softmax_scale, const void* bank_k, const void* bank_v,
+                               int32_t n_frames, const int32_t* frame_index, void* stream) {
   if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
   if (!q || !k_cur || !v_cur || !out)
     return fail(FF_ERR_INVALID_ARG, "q, k_cur, v_cur and out must be non-NULL");
@@ -286,6 +291,32 @@ ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int6
   if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
     return fail(FF_ERR_INVALID_ARG, "softmax_scale must be positive and finite");
   const ff_cache_desc& d = cache->desc;
+  const int G = d.grid_h * d.grid_w;
+  const int heads = d.num_heads;
+  const int D = d.head_dim;
+  // bank frames: distinct indices, grouped into runs of consecutive frames
+  std::vector<std::pair<int, int>> runs;
+  if (bank_k) {
+    if (n_frames < 0 || n_frames > FF_MAX_ANCHOR_FRAMES)
+      return fail(FF_ERR_RANGE, "n_frames %d outside [0, %d]", n_frames, FF_MAX_ANCHOR_FRAMES);
+    if (n_frames > 0 && (!frame_index || !bank_v))
+      return fail(FF_ERR_INVALID_ARG, "bank_v and frame_index must be non-NULL");
+    if (check_aligned(bank_k, "bank_k") != FF_OK ||
+        (n_frames > 0 && check_aligned(bank_v, "bank_v") != FF_OK))
+      return FF_ERR_INVALID_ARG;
+    std::vector<int> f(frame_index, frame_index + n_frames);
+    std::sort(f.begin(), f.end());
+    for (int j = 0; j < n_frames; ++j) {
+      if (f[j] < 0) return fail(FF_ERR_RANGE, "frame index %d < 0", f[j]);
+      if (j > 0 && f[j] == f[j - 1]) return fail(FF_ERR_INVALID_ARG, "frame %d listed twice", f[j]);
+      if (!runs.empty() && runs.back().first + runs.back().second == f[j]) ++runs.back().second;
+      else runs.push_back({f[j], 1});
+    }
+    const int64_t row = int64_t(cache->layout.elem_bytes) * heads * D;
+    for (auto& rr : runs)
+      if (int64_t(rr.second) * G * row > int64_t(UINT32_MAX))
+        return fail(FF_ERR_UNSUPPORTED, "a run of %d bank frames spans more than 4 GiB", rr.second);
+  }
   const size_t r = cache->ring_index(stage, layer);
   const int64_t expected = cache->next_chunk[r];
   if (expected >= 0 && chunk_index != expected)
@@ -293,8 +324,6 @@ ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int6
                 "attention of chunk %lld at (stage %d, layer %d); the ring holds chunks up to %lld",
                 (long long)chunk_index, stage, layer, (long long)(expected - 1));
   const int W = d.ring_chunks;
-  const int heads = d.num_heads;
-  const int D = d.head_dim;
   const int chunk_tokens = int(cache->layout.chunk_tokens);
 
   ff::KvSegments segs;
@@ -308,11 +337,20 @@ ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int6
     s.len = len;
     segs.total += len;
   };
-  // anchors: head-major, max_anchor_frames * G token stride per head
-  const int n_anchor = cache->anchor_count[layer];
-  if (n_anchor > 0)
-    add(cache->anchor_k(layer), cache->anchor_v(layer), int64_t(cache->layout.anchor_tokens) * D, D,
-        n_anchor * d.grid_h * d.grid_w);
+  if (bank_k) {
+    // bank runs: token-major
+    const int64_t row = int64_t(cache->layout.elem_bytes) * heads * D;
+    for (auto& rr : runs)
+      add(static_cast<const char*>(bank_k) + int64_t(rr.first) * G * row,
+          static_cast<const char*>(bank_v) + int64_t(rr.first) * G * row, D, heads * D,
+          rr.second * G);
+  } else {
+    // the layer's anchor segment: head-major, max_anchor_frames * G token stride per head
+    const int n_anchor = cache->anchor_count[layer];
+    if (n_anchor > 0)
+      add(cache->anchor_k(layer), cache->anchor_v(layer), int64_t(cache->layout.anchor_tokens) * D,
+          D, n_anchor * G);
+  }
   // history: chunks max(0, i - W) .. i - 1 that the ring holds, in chunk order
   for (int64_t c = chunk_index - W; c < chunk_index; ++c) {
     if (c < 0) continue;
@@ -332,6 +370,25 @@ ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int6
     e = ff::launch_attention_f32(q, out, chunk_tokens, heads, D, softmax_scale, segs,
                                  static_cast<hipStream_t>(stream));
   return hip_status(e, "chunk_attention launch");
+}
+
+}  // namespace
+
+ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
+                             const void* q, const void* k_cur, const void* v_cur, void* out,
+                             float softmax_scale, void* stream) {
+  return chunk_attention_impl(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
+                              softmax_scale, nullptr, nullptr, 0, nullptr, stream);
+}
+
+ff_status ff_chunk_attention_bank(ff_cache* cache, int32_t stage, int32_t layer,
+                                  int64_t chunk_index, const void* q, const void* k_cur,
+                                  const void* v_cur, void* out, float softmax_scale,
+                                  const void* bank_k, const void* bank_v, int32_t n_frames,
+                                  const int32_t* frame_index, void* stream) {
+  if (!bank_k) return fail(FF_ERR_INVALID_ARG, "bank_k must be non-NULL");
+  return chunk_attention_impl(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
+                              softmax_scale, bank_k, bank_v, n_frames, frame_index, stream);
 }
 
 ff_status ff_cache_ring_state(const ff_cache* cache, int32_t stage, int32_t layer,

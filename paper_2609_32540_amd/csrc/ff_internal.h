@@ -9,13 +9,15 @@
 
 namespace ff {
 
-// Keys of one attention call come as a list of segments: the anchor segment,
-// the valid history slots in chunk order, and the current chunk.  Token t of a
-// segment, head h, element e lives at element offset
+// Keys of one attention call come as a list of segments: the anchor segment
+// (or runs of consecutive frames of a caller's anchor bank), the valid history
+// slots in chunk order, and the current chunk.  Token t of a segment, head h,
+// element e lives at element offset
 //   h * head_stride + t * tok_stride + e
 // from k (and v).  Anchor and ring slots are head-major ([heads][tokens][d]);
-// the current chunk is token-major ([tokens][heads][d]).
-constexpr int kMaxSegments = 2 + FF_MAX_RING_CHUNKS;
+// the current chunk and a bank are token-major ([tokens][heads][d]).
+constexpr int kMaxSegments = FF_MAX_ANCHOR_FRAMES + FF_MAX_RING_CHUNKS + 1;
+static_assert(kMaxSegments <= 64, "the segment table lives in one lane per segment");
 
 struct KvSegment {
   const void* k;

@@ -75,6 +75,8 @@ SIGNATURES = [
     ("ff_kv_publish", _I32, [_VP, _I32, _I32, _I64, _VP, _VP, _VP]),
     ("ff_anchor_set", _I32, [_VP, _I32, _I32, _PI32, _VP, _VP, _VP]),
     ("ff_chunk_attention", _I32, [_VP, _I32, _I32, _I64, _VP, _VP, _VP, _VP, ctypes.c_float, _VP]),
+    ("ff_chunk_attention_bank", _I32, [_VP, _I32, _I32, _I64, _VP, _VP, _VP, _VP, ctypes.c_float,
+                                       _VP, _VP, _I32, _PI32, _VP]),
     ("ff_cache_ring_state", _I32, [_VP, _I32, _I32, _PI64, _PI64]),
     ("ff_cache_anchor_state", _I32, [_VP, _I32, _PI32, _PI32]),
     ("ff_cache_read", _I32, [_VP, _I32, _I32, _I32, _VP, _VP, _VP]),
@@ -220,6 +222,34 @@ class RendererCache:
             scale = 1.0 / math.sqrt(self.head_dim)
         _check(lib().ff_chunk_attention(self._h, stage, layer, chunk, qp, kp, vp, op,
                                         ctypes.c_float(scale), _stream_handle(self.device, stream)))
+        return out
+
+    def chunk_attention_bank(self, stage: int, layer: int, chunk: int, q: torch.Tensor,
+                             k: torch.Tensor, v: torch.Tensor, bank_k: torch.Tensor,
+                             bank_v: torch.Tensor, frames: Sequence[int],
+                             out: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+                             stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        """ff_chunk_attention_bank: anchors = bank frames `frames` (indices into the bank,
+        a token-major [n_bank_frames * G][heads][d] array) instead of the anchor segment."""
+        qp = self._tensor(q, self.chunk_tokens, "q")
+        kp = self._tensor(k, self.chunk_tokens, "k")
+        vp = self._tensor(v, self.chunk_tokens, "v")
+        if out is None:
+            out = torch.empty_like(q)
+        op = self._tensor(out, self.chunk_tokens, "out")
+        if bank_k.shape[0] % self.tokens_per_frame:
+            raise ValueError("the bank must hold whole frames")
+        bk = self._tensor(bank_k, bank_k.shape[0], "bank_k")
+        bv = self._tensor(bank_v, bank_k.shape[0], "bank_v")
+        n_bank = bank_k.shape[0] // self.tokens_per_frame
+        if any(not 0 <= f < n_bank for f in frames):
+            raise ValueError(f"bank frame index out of range [0, {n_bank})")
+        fr = (ctypes.c_int32 * max(len(frames), 1))(*frames)
+        if scale is None:
+            scale = 1.0 / math.sqrt(self.head_dim)
+        _check(lib().ff_chunk_attention_bank(self._h, stage, layer, chunk, qp, kp, vp, op,
+                                             ctypes.c_float(scale), bk, bv, len(frames), fr,
+                                             _stream_handle(self.device, stream)))
         return out
 
     # ------------------------------------------------------------------

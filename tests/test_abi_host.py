@@ -34,7 +34,7 @@ def desc(**kw):
 def test_library_exports_every_header_symbol():
     L = ff.lib()
     names = header_functions()
-    assert len(names) == 18
+    assert len(names) == 19
     for n in names:
         assert hasattr(L, n), n
     assert {n for n, _, _ in ff.SIGNATURES} == set(names)

@@ -42,11 +42,14 @@ def test_euler_step_bit_exact(dtype, n):
 SIGMAS = [1.0, 0.75, 0.5, 0.25, 0.0]      # S = 4 stages, sigma_S > ... > sigma_0 = 0
 
 
-def make_stub(cache, w, X, layers):
+def make_stub(cache, w, X, layers, bank=None):
     """One renderer forward of rank s (the paper's k = S - s) on chunk i, on
     `stream`: per layer, Q/K/V from the current hidden state, RoPE, attention
     over [anchors | ring of stage s | chunk], publish; the last layer's output
-    is the velocity of the Euler step that hands x_{i,k-1} on in place."""
+    is the velocity of the Euler step that hands x_{i,k-1} on in place.  With
+    a bank (per layer: K, V, latent frame of each bank frame), chunk i reads
+    its window Gamma(i) from it, so ranks busy with different chunks read
+    different windows at the same time."""
     S = len(SIGMAS) - 1
 
     def forward(s, i, stream):
@@ -58,7 +61,12 @@ def make_stub(cache, w, X, layers):
                 k = (h * 0.5).to(h.dtype)
                 v = (h + 0.25).to(h.dtype)
                 cache.rope3d(q, k, frames, stream=stream)
-                h = cache.chunk_attention(s, l, i, q, k, v, stream=stream)
+                if bank is None:
+                    h = cache.chunk_attention(s, l, i, q, k, v, stream=stream)
+                else:
+                    bk, bv, bframes = bank[l]
+                    idx = [bframes.index(f) for f in w.anchor_frames_for_chunk(i)]
+                    h = cache.chunk_attention_bank(s, l, i, q, k, v, bk, bv, idx, stream=stream)
                 cache.kv_publish(s, l, i, k, v, stream=stream)
             k_idx = S - s
             ff.euler_step(X[i], h, SIGMAS[k_idx] - SIGMAS[k_idx - 1], out=X[i], stream=stream)
@@ -119,3 +127,64 @@ def test_wavefront_equals_chunk_major(N_R, layers):
                 kb, vb = cache_b.read(s, l, slot)
                 torch.cuda.synchronize()
                 assert torch.equal(ka, kb) and torch.equal(va, vb)
+
+
+def test_wavefront_with_anchor_windows_from_a_bank():
+    """27 chunks x 4 stages of a reduced 480p-like grid with the window rule
+    Gamma(i): ranks read different windows at the same time from the bank;
+    bit-identical to the chunk-major run, and each chunk's first-stage output
+    equals the anchor-segment path when its window is set as the segment."""
+    S = len(SIGMAS) - 1
+    N_R = 27
+    w = synth.small_workload("wave-bank", dtype="bf16", heads=2, head_dim=128, grid_h=4,
+                             grid_w=7, ring_chunks=4, stages=S, layers=1, n_chunks=N_R,
+                             anchor_rule="window", max_anchor_frames=3)
+    frames = sorted({f for i in range(N_R) for f in w.anchor_frames_for_chunk(i)})
+    assert len({tuple(w.anchor_frames_for_chunk(i)) for i in range(N_R)}) > 2
+    ak, av = synth.anchor_tensors(w, frames, 0)
+    akd, avd = to_dev(ak), to_dev(av)
+    G = w.tokens_per_frame
+    # rotate each bank frame at its own latent position (frames are not one run of positions)
+    for n, f in enumerate(frames):
+        sl = slice(n * G, (n + 1) * G)
+        kf = akd[sl].clone()
+        make_cache(w, stages=1, layers=1).rope3d(None, kf, [f])
+        akd[sl] = kf
+    bank = {0: (akd, avd, frames)}
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    noise = [torch.randn((w.chunk_tokens, w.heads, w.head_dim), generator=g, device=dev)
+             .to(torch.bfloat16) for _ in range(N_R)]
+    torch.cuda.synchronize()
+    cache_a, X_a = make_cache(w, stages=S, layers=1), [t.clone() for t in noise]
+    fwd_a = make_stub(cache_a, w, X_a, 1, bank)
+    s0 = torch.cuda.Stream()
+    for i in range(N_R):
+        for s in range(S):
+            fwd_a(s, i, s0)
+    torch.cuda.synchronize()
+    cache_b, X_b = make_cache(w, stages=S, layers=1), [t.clone() for t in noise]
+    streams = [torch.cuda.Stream() for _ in range(S)]
+    rounds, forwards = ff.wavefront_run(N_R, streams, make_stub(cache_b, w, X_b, 1, bank))
+    torch.cuda.synchronize()
+    assert (rounds, forwards) == (N_R + S - 1, N_R * S)
+    for i in range(N_R):
+        np.testing.assert_array_equal(exact(X_b[i]), exact(X_a[i]))
+    # bank path == anchor-segment path, bit for bit, on fresh rings (stage 0 only)
+    c1, c2 = make_cache(w, stages=1, layers=1), make_cache(w, stages=1, layers=1)
+    cur = None
+    for i in range(N_R):
+        q, k, v = (to_dev(synth.chunk_tensor(w, t, i, 0, 0)) for t in (synth.T_Q, synth.T_K, synth.T_V))
+        win = w.anchor_frames_for_chunk(i)
+        idx = [frames.index(f) for f in win]
+        if win != cur:
+            c2.anchor_set(0, win, torch.cat([akd[j * G:(j + 1) * G] for j in idx]).contiguous(),
+                          torch.cat([avd[j * G:(j + 1) * G] for j in idx]).contiguous())
+            cur = win
+        o1 = c1.chunk_attention_bank(0, 0, i, q, k, v, akd, avd, idx)
+        o2 = c2.chunk_attention(0, 0, i, q, k, v)
+        c1.kv_publish(0, 0, i, k, v)
+        c2.kv_publish(0, 0, i, k, v)
+        torch.cuda.synchronize()
+        assert torch.equal(o1, o2), i
