@@ -22,15 +22,20 @@
 //                   transposing LDS read (ds_read_b64_tr_b16); B = P^T, the
 //                   softmax registers rounded to bf16 in place.  The keys of each
 //                   8-key operand are chosen to match the accumulator layout.
-// Software pipeline (besides the second wave on each SIMD, the overlap is built
-// into each wave's instruction stream): while the matrix core computes the first half of
-// S^T of tile t+1, the VALU exponentiates the first half of tile t; while it
-// accumulates that half into O^T, the VALU exponentiates the second half; the
-// second halves of S^T(t+1) and of O^T follow, with the column max of tile t+1.
+// Software pipeline: while the matrix core computes block 0 of S^T of tile
+// t+1, the VALU exponentiates tile t (h1); the products of tile t into O^T,
+// block 1 of S^T(t+1) and the column max of tile t+1 follow (h2).  Waves w and
+// w + 4 share a SIMD: waves 0-3 run h1(t) h2(t) after barrier t, waves 4-7 run
+// h2(t-1) h1(t), half an iteration later, so on every SIMD one wave's
+// exponentials run beside the other's matrix work instead of both waves
+// wanting the same unit at once.
 // K and V tiles are copied from HBM straight into LDS (global_load_lds_dwordx4,
-// 16 bytes per lane, issued by waves 0-3) two tiles ahead, into a ring of three
-// tile slots: one barrier per tile.  The loop is unrolled by three so every slot reference is
-// static (reads of one slot are never ordered behind the copy into another).
+// 16 bytes per lane, issued by waves 0-3) two tiles ahead, into a ring of four
+// tile slots: one barrier per tile (plus one at the end).  The last reads of
+// tile t (h2(t) of waves 4-7) come before barrier t+2, where tile t+4 is
+// copied into its slot.  The loops are unrolled by four so every slot
+// reference is static (reads of one slot are never ordered behind the copy
+// into another).
 // Tile rows are stored without padding, with an XOR swizzle of their 16-byte
 // chunks that keeps both the K reads and the transposing V reads free of bank
 // conflicts on the 64-bank LDS.
@@ -139,6 +144,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
   __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
   __shared__ __attribute__((aligned(1024))) char lds2[C::SLOT];
+  __shared__ __attribute__((aligned(1024))) char lds3[C::SLOT];
 
   // XCD-aware renumbering: hardware block b runs on XCD b % 8; give each XCD a
   // contiguous range of logical tiles.
@@ -393,49 +399,84 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   update_max(s_cur);
   c_next = advance(c_next);                  // tile 1
 
-  // ---- main loop: iteration t finishes tile t and computes S^T of tile t+1 -----------
-  // tile t sits in slot t % 3: its V is read from v_slot, the K of tile t+1 from
-  // k_slot, and tile t+2 is copied into dma_slot (tile t-1's, free after the barrier).
-  auto iteration = [&](int t, char* v_slot, char* k_slot, char* dma_slot) {
-    const bool has_next = t + 1 < n_tiles;
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of tile t+1 have landed
-    __syncthreads();                // everyone's have; everyone is done with tile t-1
-    if (t + 2 < n_tiles) issue_tile(dma_slot, c_dma);
-    // keep the per-read address arithmetic inside the loop (no hoisted copies)
+  // ---- main loop, in two halves per tile ---------------------------------------
+  // h1(t): S^T block 0 of tile t+1, P^T of tile t, O^T += block 0 of tile t.
+  // h2(t): S^T block 1 of tile t+1, O^T += block 1 of tile t, column max of t+1.
+  // Waves 0-3 run [barrier t, copy of tile t+2, h1(t), h2(t)]; waves 4-7, which
+  // share their SIMDs, run half an iteration later, [barrier t, h2(t-1), h1(t)],
+  // so each SIMD pairs one wave's exponentials with the other's matrix work.
+  // Tile t lives in slot t % 4; the last reads of tile t (waves 4-7, h2(t))
+  // precede barrier t+2, where waves 0-3 copy tile t+4 into its slot.
+  f32x16 s_nxt[2][kCB];
+  uint32_t pk0[kCB][8], pk1[kCB][8];
+  auto h1 = [&](char* v_slot, char* k_slot) __attribute__((always_inline)) {
     asm volatile("" : "+v"(k_lane), "+v"(v_lane[0]), "+v"(v_lane[1]));
-    // (past the last tile the S^T products read a stale slot and are discarded)
-    f32x16 s_nxt[2][kCB];
-    uint32_t pk0[kCB][8], pk1[kCB][8];
-    // block 0 of S^T(t+1) on the matrix core while the VALU exponentiates block 0 of tile t
     compute_s(k_slot, 0, s_nxt);
     probs(s_cur, 0, pk0);
-    // block 0 of tile t into O^T while the VALU exponentiates block 1 of tile t
     pv(v_slot + C::TILE, 0, pk0);
     probs(s_cur, 1, pk1);
-    // block 1 of S^T(t+1), then block 1 of tile t into O^T, while the VALU takes
-    // the column max of tile t+1
+  };
+  auto h2 = [&](int t, char* v_slot, char* k_slot) __attribute__((always_inline)) {
+    asm volatile("" : "+v"(k_lane), "+v"(v_lane[0]), "+v"(v_lane[1]));
     compute_s(k_slot, 1, s_nxt);
     pv(v_slot + C::TILE, 1, pk1);
-    if (has_next) {
+    if (t + 1 < n_tiles) {
       const int nv = min(kBK, seg_len(c_next.sg) - c_next.k0);
       if (nv < kBK) mask_s(s_nxt, nv);
       update_max(s_nxt);
+      c_next = advance(c_next);
     }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int cb = 0; cb < kCB; ++cb) s_cur[kb][cb] = s_nxt[kb][cb];
-    if (has_next) c_next = advance(c_next);
-    if (t + 2 < n_tiles) c_dma = advance(c_dma);
   };
-
-  for (int t = 0; t < n_tiles;) {
-    iteration(t, lds0, lds1, lds2);
-    if (++t >= n_tiles) break;
-    iteration(t, lds1, lds2, lds0);
-    if (++t >= n_tiles) break;
-    iteration(t, lds2, lds0, lds1);
-    ++t;
+  // barrier t: every wave's copies of tile t+1 have landed, tile t-2 is free
+  auto sync = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  };
+  if (wave < kCopyWaves) {
+    auto step = [&](int t, char* s0, char* s1, char* s2) __attribute__((always_inline)) {
+      sync();
+      if (t + 2 < n_tiles) {
+        issue_tile(s2, c_dma);
+        c_dma = advance(c_dma);
+      }
+      h1(s0, s1);
+      h2(t, s0, s1);
+    };
+    for (int t = 0; t < n_tiles;) {
+      step(t, lds0, lds1, lds2);
+      if (++t >= n_tiles) break;
+      step(t, lds1, lds2, lds3);
+      if (++t >= n_tiles) break;
+      step(t, lds2, lds3, lds0);
+      if (++t >= n_tiles) break;
+      step(t, lds3, lds0, lds1);
+      ++t;
+    }
+    sync();   // matches the extra barrier of the last step of waves 4-7
+  } else {
+    sync();
+    h1(lds0, lds1);
+    // step t: barrier t, h2(t-1), and h1(t) while t < n_tiles; the step with
+    // t = n_tiles only finishes the last tile
+    auto step = [&](int t, char* sp, char* s0, char* s1) __attribute__((always_inline)) {
+      sync();
+      h2(t - 1, sp, s0);
+      if (t < n_tiles) h1(s0, s1);
+    };
+    for (int t = 1;;) {
+      step(t, lds0, lds1, lds2);
+      if (t++ >= n_tiles) break;
+      step(t, lds1, lds2, lds3);
+      if (t++ >= n_tiles) break;
+      step(t, lds2, lds3, lds0);
+      if (t++ >= n_tiles) break;
+      step(t, lds3, lds0, lds1);
+      if (t++ >= n_tiles) break;
+    }
   }
 
   // normalise and store: register j of block db holds d = 32 db + 8 (j / 4) + 4 half + j % 4
