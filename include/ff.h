@@ -250,12 +250,41 @@ typedef struct {
  * [heads][head_dim] (may be NULL without anchor frames).  Equals
  * ff_chunk_attention of chunk i after chunks 0 .. i-1 were published into a
  * ring of W = window (same precision rules).  Tensor pointers must be
- * 16-byte aligned (FF_ERR_INVALID_ARG).  A run of the read set (one chunk window, or
+ * 16-byte aligned (FF_ERR_INVALID_ARG).  lse (optional, device,
+ * [n_chunks * chunk_tokens][heads] float, bf16 path only) receives each
+ * query's base-2 log-sum-exp of scale * log2(e) * q.k over its visible keys,
+ * the statistic ff_packed_attention_bwd needs.  A run of the read set (one chunk window, or
  * consecutive anchor frames) may span at most 2^32 - 1 bytes
  * (FF_ERR_UNSUPPORTED).  Host validation only; one kernel launch. */
 ff_status ff_packed_attention(const ff_packed_desc* desc, const void* q, const void* k,
                               const void* v, const void* anchor_k, const void* anchor_v,
-                              void* out, float softmax_scale, void* stream);
+                              void* out, float softmax_scale, float* lse, void* stream);
+
+/* Device workspace bytes of ff_packed_attention_bwd for `desc`
+ * (n_chunks * chunk_tokens * num_heads floats); 0 for an invalid desc. */
+size_t ff_packed_attention_bwd_workspace(const ff_packed_desc* desc);
+
+/* Backward pass of ff_packed_attention (bf16 only): given the forward's
+ * inputs, its output `out`, the output gradient `dout` (both [n_chunks *
+ * chunk_tokens][heads][head_dim]) and its log-sum-exp `lse`, writes
+ * dq, dk, dv (shapes of q, k, v) and d_anchor_k, d_anchor_v (shape of the
+ * anchor arrays; gradients summed over every chunk that sees the frame; zero
+ * for frames no chunk sees):
+ *   P = softmax(scale Q K^T) over the visible keys, dV = P^T dO,
+ *   dS = P * (dO V^T - rowsum(dO * O)), dQ = scale dS K, dK = scale dS^T Q,
+ * with products on bf16 matrix cores, float32 accumulation, P and dS rounded
+ * to bf16 as operands and every gradient rounded once to bf16.  Gradient of
+ * the packed training forward through its KV edges (App. Alg. 2).
+ * `workspace` (device, ff_packed_attention_bwd_workspace() bytes, 16-byte
+ * aligned) holds rowsum(dO * O).  At most 64 anchor frames, and the chunks
+ * that see one frame may form at most 8 runs of consecutive chunks
+ * (FF_ERR_UNSUPPORTED).  Host validation, then four launches. */
+ff_status ff_packed_attention_bwd(const ff_packed_desc* desc, const void* q, const void* k,
+                                  const void* v, const void* anchor_k, const void* anchor_v,
+                                  const void* out, const void* dout, const float* lse, void* dq,
+                                  void* dk, void* dv, void* d_anchor_k, void* d_anchor_v,
+                                  float softmax_scale, void* workspace, size_t workspace_bytes,
+                                  void* stream);
 
 /* Anchor partition of a clip of L latent frames with anchor spacing delta
  * (Eq. anchor-infill-partition): P = {m * delta : m * delta < L} u {L - 1},

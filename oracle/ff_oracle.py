@@ -336,6 +336,57 @@ def packed_stage_attention(Qs: Sequence[np.ndarray], Ks: Sequence[np.ndarray],
     return outs
 
 
+def packed_visibility(n_chunks: int, chunk_tokens: int, frame_tokens: int, n_frames: int,
+                      anchors_of_chunk: Sequence[Sequence[int]], W: int) -> np.ndarray:
+    """Boolean mask [n_chunks*chunk_tokens, n_frames*frame_tokens + n_chunks*chunk_tokens]
+    of the packed sequence [anchor frames | chunk 0 | chunk 1 | ...]: the renderer
+    rows of the packed training mask (chunk i sees chunks max(0, i-W) .. i and its
+    listed anchor frames)."""
+    n_anchor = n_frames * frame_tokens
+    M = np.zeros((n_chunks * chunk_tokens, n_anchor + n_chunks * chunk_tokens), bool)
+    for i in range(n_chunks):
+        rows = slice(i * chunk_tokens, (i + 1) * chunk_tokens)
+        for f in anchors_of_chunk[i]:
+            M[rows, f * frame_tokens:(f + 1) * frame_tokens] = True
+        M[rows, n_anchor + max(0, i - W) * chunk_tokens:n_anchor + (i + 1) * chunk_tokens] = True
+    return M
+
+
+def masked_attention_grad(Q: np.ndarray, K: np.ndarray, V: np.ndarray, visible: np.ndarray,
+                          dO: np.ndarray, scale: float):
+    """Gradients of O = softmax(scale Q K^T, masked) V with respect to Q, K, V, per head,
+    in float64, from the definitions: P = softmax, dV = P^T dO, dP = dO V^T,
+    dS = P * (dP - rowsum(dP * P)), dQ = scale dS K, dK = scale dS^T Q.
+    Q [n][h][d], K, V [m][h][d], visible [n][m] bool, dO [n][h][d]."""
+    Q, K, V, dO = (np.asarray(a, np.float64) for a in (Q, K, V, dO))
+    dQ, dK, dV = np.zeros_like(Q), np.zeros_like(K), np.zeros_like(V)
+    for h in range(Q.shape[1]):
+        s = scale * (Q[:, h] @ K[:, h].T)
+        s = np.where(visible, s, -np.inf)
+        s = s - s.max(axis=1, keepdims=True)
+        P = np.exp(s)
+        P = P / P.sum(axis=1, keepdims=True)
+        dV[:, h] = P.T @ dO[:, h]
+        dP = dO[:, h] @ V[:, h].T
+        dS = P * (dP - (dP * P).sum(axis=1, keepdims=True))
+        dQ[:, h] = scale * (dS @ K[:, h])
+        dK[:, h] = scale * (dS.T @ Q[:, h])
+    return dQ, dK, dV
+
+
+def log2_sum_exp2(Q: np.ndarray, K: np.ndarray, visible: np.ndarray, scale: float) -> np.ndarray:
+    """Per query and head, log2 of sum_j 2^(scale log2(e) q.k_j) over visible keys
+    (the forward's base-2 log-sum-exp): [n][h]."""
+    Q, K = np.asarray(Q, np.float64), np.asarray(K, np.float64)
+    out = np.empty((Q.shape[0], Q.shape[1]))
+    for h in range(Q.shape[1]):
+        s = (scale * np.log2(np.e)) * (Q[:, h] @ K[:, h].T)
+        s = np.where(visible, s, -np.inf)
+        m = s.max(axis=1, keepdims=True)
+        out[:, h] = (m + np.log2(np.exp2(s - m).sum(axis=1, keepdims=True)))[:, 0]
+    return out
+
+
 # --------------------------------------------------------------------------
 # Sampler step and the wavefront schedule
 # --------------------------------------------------------------------------

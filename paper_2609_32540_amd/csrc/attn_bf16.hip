@@ -483,7 +483,13 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
 #pragma unroll
   for (int cb = 0; cb < kCB; ++cb) {
     const int qi = q0 + 32 * cb + l32;
-    const float inv = 1.0f / sum_across_halves(l_run[cb]);
+    const float l_tot = sum_across_halves(l_run[cb]);
+    const float inv = 1.0f / l_tot;
+    if constexpr (kPacked) {
+      // base-2 log-sum-exp of the scaled logits, for the backward pass
+      if (src.lse != nullptr && half == 0 && qi < nq)
+        src.lse[(int64_t(chunk) * nq + qi) * heads + head] = m_run[cb] + log2f(l_tot);
+    }
     if (qi < nq) {
       __bf16* op = out + (int64_t(qi) * heads + head) * D + 4 * half;
 #pragma unroll

@@ -1,0 +1,539 @@
+// Backward pass of the packed block-causal attention (bf16 in and out, float32
+// accumulation), the gradient of the packed training forward through its KV
+// edges.  With c = scale * log2(e) and the forward's base-2 log-sum-exp L_i:
+//   P_ij  = 2^(c q_i.k_j - L_i)                 (visible pairs only)
+//   D_i   = dO_i . O_i
+//   dV_j  = sum_i P_ij dO_i
+//   dS_ij = P_ij (dO_i . v_j - D_i)
+//   dQ_i  = scale sum_j dS_ij k_j
+//   dK_j  = scale sum_i dS_ij q_i
+// Four launches: D; dQ (query-stationary: a workgroup holds 256 queries of one
+// chunk and head and streams the 64-key tiles of their read set, like the
+// forward); dV and dK (key-stationary: a workgroup holds 256 keys of one chunk
+// or anchor frame and head and streams the 64-query tiles of every chunk that
+// sees them).  Every output element is written by exactly one workgroup: no
+// atomics.
+//
+// Products on v_mfma_f32_32x32x16_bf16 with the forward's operand layouts: the
+// stationary side (Q^T and dO^T, or K^T and V^T) sits in registers as the B
+// operand, tiles of the streamed side are copied HBM -> LDS (global_load_lds)
+// one tile ahead into a two-slot ring and read as the A operand (16-byte rows)
+// or, transposed, with ds_read_b64_tr_b16; P and dS go from the accumulators to
+// the B operand of the next product as bf16 (nearest even).
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+
+#include <cstring>
+
+#include "ff_internal.h"
+
+namespace ff {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+#define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
+#define GLOBAL_PTR(p) ((const __attribute__((address_space(1))) void*)(p))
+
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kBlockN = 32 * kWaves;   // stationary columns (queries or keys) per workgroup
+constexpr int kBT = 64;                // streamed rows per tile
+constexpr int kXcds = 8;
+constexpr int kMaxRuns = 2 * FF_MAX_ANCHOR_FRAMES + 1;   // segments of one streamed set
+
+template <int D>
+struct Cfg {
+  static constexpr int KS = D / 16;
+  static constexpr int DB = D / 32;
+  static constexpr int ROWB = 2 * D;
+  static constexpr int CPR = D / 8;
+  static constexpr int RPB = 1024 / ROWB;
+  static constexpr int BLOCKS = kBT / RPB;              // 1 KB copies per tile and tensor
+  static constexpr int BLOCKS_PER_WAVE = BLOCKS / kWaves;
+  static constexpr int TILE = kBT * ROWB;
+  static constexpr int VEC = kBT * 4;                   // one float per streamed row
+  static constexpr int SLOT = 2 * TILE + 2 * VEC;       // tensor A, tensor B, vector A, vector B
+  static_assert(BLOCKS % kWaves == 0, "every wave copies the same number of 1 KB blocks");
+};
+
+// the forward's LDS swizzle (conflict-free 16-byte row reads and transposing reads)
+template <int D>
+__device__ inline int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
+
+__device__ inline uint32_t pack_bf16(float a, float b) {
+  f32x2 f = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+}
+
+__device__ inline uint64_t readlane_u64(uint64_t v, int lane) {
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), lane));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v >> 32)), lane));
+  return (uint64_t(hi) << 32) | uint64_t(lo);
+}
+
+// Streams the tiles of up to kMaxRuns runs of rows through a two-slot LDS
+// ring.  Run i (held by lane i, read with v_readlane): `len` rows of two
+// token-major tensors (row r at a + r * row_bytes and b + r * row_bytes, this
+// head's columns) and, with kVec, two float vectors (element r at
+// va + r * vec_bytes and vb + r * vec_bytes).
+template <int D, bool kVec>
+struct Stream {
+  using C = Cfg<D>;
+  int len = 0;
+  uint64_t a = 0, b = 0, va = 0, vb = 0;
+  uint32_t row_bytes, vec_bytes;
+  int n_runs, n_tiles;
+  int sg = 0, k0 = 0;    // tile being copied next
+  int cp_row[C::BLOCKS_PER_WAVE], cp_choff[C::BLOCKS_PER_WAVE];
+  int wave, lane;
+
+  __device__ int run_len(int i) const { return __builtin_amdgcn_readlane(len, i); }
+  __device__ void advance(int& s, int& k) const {
+    k += kBT;
+    if (k >= run_len(s)) {
+      ++s;
+      k = 0;
+    }
+  }
+  // copy the next tile into `slot` (rows past a partial tile's end repeat its last row)
+  __device__ void issue(char* slot) {
+    const int n = run_len(sg);
+    const char* ga = reinterpret_cast<const char*>(readlane_u64(a, sg));
+    const char* gb = reinterpret_cast<const char*>(readlane_u64(b, sg));
+    const bool partial = k0 + kBT > n;
+#pragma unroll
+    for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
+      int tok = k0 + cp_row[i];
+      if (partial) tok = min(tok, n - 1);
+      const uint32_t off = uint32_t(tok) * row_bytes + uint32_t(cp_choff[i]);
+      char* dst = slot + (wave * C::BLOCKS_PER_WAVE + i) * 1024;
+      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(ga + off), LDS_PTR(void, dst), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(gb + off), LDS_PTR(void, dst + C::TILE), 16, 0, 0);
+    }
+    if constexpr (kVec) {
+      if (wave == 0) {
+        const char* pa = reinterpret_cast<const char*>(readlane_u64(va, sg));
+        const char* pb = reinterpret_cast<const char*>(readlane_u64(vb, sg));
+        const uint32_t off = uint32_t(min(k0 + lane, n - 1)) * vec_bytes;
+        __builtin_amdgcn_global_load_lds(GLOBAL_PTR(pa + off), LDS_PTR(void, slot + 2 * C::TILE), 4, 0, 0);
+        __builtin_amdgcn_global_load_lds(GLOBAL_PTR(pb + off), LDS_PTR(void, slot + 2 * C::TILE + C::VEC), 4, 0, 0);
+      }
+    }
+    advance(sg, k0);
+  }
+};
+
+// acc[kb] = A(rows kb*32 .. +31 of the tile) x B^T, B the stationary operand
+// (lane (l32, half) holds column l32, elements 16 ks + 8 half .. +7)
+template <int D>
+__device__ inline void rows_times_b(const char* tile, int kb, int a_lane, const bf16x8 (&breg)[D / 16],
+                                    f32x16& acc) {
+#pragma unroll
+  for (int j = 0; j < 16; ++j) acc[j] = 0.0f;
+  const char* base = tile + kb * 32 * Cfg<D>::ROWB;
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    const bf16x8 a = *reinterpret_cast<const bf16x8*>(base + (a_lane ^ (ks << 5)));
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, breg[ks], acc, 0, 0, 0);
+  }
+}
+
+// out[db] += (rows kb*32 .. +31 of the tile)^T x P, P packed bf16 from the
+// accumulator layout (register j of the block = row 8 (j/4) + 4 half + j%4)
+template <int D>
+__device__ inline void rows_t_times_p(const char* tile, int kb, const int (&t_lane)[2],
+                                      const uint32_t (&pk)[8], f32x16 (&out)[D / 32]) {
+#pragma unroll
+  for (int mh = 0; mh < 2; ++mh) {
+    const u32x4 pu = {pk[4 * mh + 0], pk[4 * mh + 1], pk[4 * mh + 2], pk[4 * mh + 3]};
+    const bf16x8 pb = __builtin_bit_cast(bf16x8, pu);
+    const char* base = tile + (kb * 32 + 16 * mh) * Cfg<D>::ROWB;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, base + (t_lane[0] ^ (db << 6))));
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, base + (t_lane[1] ^ (db << 6))));
+      const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
+      const u32x4 au = {lo2[0], lo2[1], hi2[0], hi2[1]};
+      out[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, au), pb, out[db], 0, 0, 0);
+    }
+  }
+}
+
+// lane address bases of the two LDS read patterns (as in the forward)
+template <int D>
+struct Lanes {
+  int a_lane;
+  int t_lane[2];
+  __device__ Lanes(int lane) {
+    const int l32 = lane & 31, half = lane >> 5;
+    a_lane = l32 * Cfg<D>::ROWB + ((half ^ swz<D>(l32)) << 4);
+    const int g = lane >> 4, lp = lane & 15;
+    const int v_row = 4 * (g >> 1) + (lp >> 2);
+    const int v_dsub = 16 * (g & 1) + 4 * (lp & 3);
+#pragma unroll
+    for (int hi = 0; hi < 2; ++hi) {
+      const int r = v_row + 8 * hi;
+      t_lane[hi] = r * Cfg<D>::ROWB + (((v_dsub >> 3) ^ swz<D>(r)) << 4) + (v_dsub & 7) * 2;
+    }
+  }
+};
+
+// load the stationary B operand of one wave: 32 columns (rows of a token-major
+// tensor, clamped to n - 1), lane (l32, half) gets elements 16 ks + 8 half .. +7
+template <int D>
+__device__ inline void load_b(const __bf16* base, int64_t row_elems, int col0, int n, int lane,
+                              bf16x8 (&breg)[D / 16]) {
+  const int r = min(col0 + (lane & 31), n - 1);
+  const __bf16* p = base + int64_t(r) * row_elems + 8 * (lane >> 5);
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) breg[ks] = *reinterpret_cast<const bf16x8*>(p + 16 * ks);
+}
+
+// store scale * acc^T: acc rows = d (32 db + 8 (j/4) + 4 half + j%4), columns = lanes
+template <int D>
+__device__ inline void store_t(__bf16* base, int64_t row_elems, int col, int n, int lane,
+                               const f32x16 (&acc)[D / 32], float scale) {
+  if (col >= n) return;
+  __bf16* p = base + int64_t(col) * row_elems + 4 * (lane >> 5);
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      u32x2 w;
+      w.x = pack_bf16(acc[db][4 * a + 0] * scale, acc[db][4 * a + 1] * scale);
+      w.y = pack_bf16(acc[db][4 * a + 2] * scale, acc[db][4 * a + 3] * scale);
+      *reinterpret_cast<u32x2*>(p + 32 * db + 8 * a) = w;
+    }
+}
+
+__device__ inline int xcd_logical(int b, int n_wg) {
+  const int xcd = b % kXcds, idx = b / kXcds;
+  const int per = n_wg / kXcds, rem = n_wg % kXcds;
+  return xcd * per + min(xcd, rem) + idx;
+}
+
+// ---- D_i = dO_i . O_i ---------------------------------------------------------------
+__global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict__ o,
+                                                        const __bf16* __restrict__ dout,
+                                                        float* __restrict__ delta, int64_t rows,
+                                                        int d) {
+  const int64_t r = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (r >= rows) return;
+  const u32x4* po = reinterpret_cast<const u32x4*>(o + r * d);
+  const u32x4* pd = reinterpret_cast<const u32x4*>(dout + r * d);
+  float acc = 0.0f;
+  for (int c = 0; c < d / 8; ++c) {
+    const u32x4 a = po[c], b = pd[c];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc = fmaf(__uint_as_float(a[j] << 16), __uint_as_float(b[j] << 16), acc);
+      acc = fmaf(__uint_as_float(a[j] & 0xffff0000u), __uint_as_float(b[j] & 0xffff0000u), acc);
+    }
+  }
+  delta[r] = acc;
+}
+
+// ---- dQ: query-stationary ---------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void bwd_dq_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout,
+                   const float* __restrict__ lse, const float* __restrict__ delta,
+                   __bf16* __restrict__ dq, int heads, float c_log2, float scale, PackedPlan plan,
+                   int n_qtiles) {
+  using C = Cfg<D>;
+  __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
+  __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
+  const int nq = plan.chunk_tokens;
+  const int logical = xcd_logical(blockIdx.x, gridDim.x);
+  const int chunk = logical / (heads * n_qtiles);
+  const int rest = logical - chunk * heads * n_qtiles;
+  const int head = rest / n_qtiles, qt = rest % n_qtiles;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l32 = lane & 31, half = lane >> 5;
+  const int64_t tok0 = int64_t(chunk) * nq;
+  const int64_t row_elems = int64_t(heads) * D;
+  const int q0 = qt * kBlockN + wave * 32;
+
+  bf16x8 qreg[C::KS], dreg[C::KS];
+  load_b<D>(q + tok0 * row_elems + head * D, row_elems, q0, nq, lane, qreg);
+  load_b<D>(dout + tok0 * row_elems + head * D, row_elems, q0, nq, lane, dreg);
+  const int qi = min(q0 + l32, nq - 1);
+  const float L = lse[(tok0 + qi) * heads + head];
+  const float Dq = delta[(tok0 + qi) * heads + head];
+  f32x16 acc[C::DB];
+#pragma unroll
+  for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[db][j] = 0.0f;
+
+  Stream<D, false> st;
+  st.wave = wave;
+  st.lane = lane;
+  st.row_bytes = uint32_t(2 * row_elems);
+  st.n_runs = packed_num_segments(plan, chunk);
+#pragma unroll
+  for (int i = 0; i < kMaxRuns; ++i)
+    if (lane == i && i < st.n_runs) {
+      const KvSegment s = packed_segment(plan, chunk, i, heads, D, 2);
+      st.len = s.len;
+      st.a = reinterpret_cast<uint64_t>(s.k) + 2ull * uint64_t(head) * D;
+      st.b = reinterpret_cast<uint64_t>(s.v) + 2ull * uint64_t(head) * D;
+    }
+  st.n_tiles = 0;
+  for (int i = 0; i < st.n_runs; ++i) st.n_tiles += (st.run_len(i) + kBT - 1) / kBT;
+#pragma unroll
+  for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
+    const int r = (wave * C::BLOCKS_PER_WAVE + i) * C::RPB + lane / C::CPR;
+    st.cp_row[i] = r;
+    st.cp_choff[i] = 16 * ((lane % C::CPR) ^ swz<D>(r));
+  }
+  Lanes<D> ln(lane);
+  int csg = 0, ck0 = 0;   // tile being computed
+
+  auto tile = [&](int t, char* cur, char* nxt) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (t + 1 < st.n_tiles) st.issue(nxt);
+    // keep the per-read address arithmetic inside the loop (no hoisted copies)
+    asm volatile("" : "+v"(ln.a_lane), "+v"(ln.t_lane[0]), "+v"(ln.t_lane[1]));
+    const int nv = min(kBT, st.run_len(csg) - ck0);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 s, dp;
+      rows_times_b<D>(cur, kb, ln.a_lane, qreg, s);              // S^T = K Q^T
+      __builtin_amdgcn_sched_barrier(0);
+      rows_times_b<D>(cur + C::TILE, kb, ln.a_lane, dreg, dp);   // dP^T = V dO^T
+      __builtin_amdgcn_sched_barrier(0);
+      uint32_t pk[8];
+#pragma unroll
+      for (int j = 0; j < 16; j += 2) {
+        float v2[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int key = kb * 32 + 8 * ((j + e) >> 2) + 4 * half + ((j + e) & 3);
+          const float p = key < nv ? __builtin_amdgcn_exp2f(fmaf(s[j + e], c_log2, -L)) : 0.0f;
+          v2[e] = p * (dp[j + e] - Dq);
+        }
+        pk[j >> 1] = pack_bf16(v2[0], v2[1]);
+      }
+      rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);            // dQ^T += K^T dS^T
+      __builtin_amdgcn_sched_barrier(0);   // one 32-key block at a time (register budget)
+    }
+    st.advance(csg, ck0);
+  };
+  if (st.n_tiles > 0) st.issue(lds0);
+  for (int t = 0; t < st.n_tiles;) {
+    tile(t, lds0, lds1);
+    if (++t >= st.n_tiles) break;
+    tile(t, lds1, lds0);
+    ++t;
+  }
+  store_t<D>(dq + tok0 * row_elems + head * D, row_elems, q0 + l32, nq, lane, acc, scale);
+}
+
+// ---- dK or dV: key-stationary -----------------------------------------------------------
+// Key units: unit u < n_chunks * kpc is keys [256 k, 256 k + 256) of chunk
+// u / kpc; the rest are anchor frames, kpf units each.  Each unit streams the
+// query runs that see it (chunks max(0, .) .. c + window of the packed clip,
+// or the chunk runs listed for the anchor frame).
+struct KeyUnits {
+  int32_t kpc, kpf, n_frames;
+  uint8_t frame_runs[FF_MAX_ANCHOR_FRAMES * 8][16];   // per anchor frame: (first chunk, count) pairs
+};
+
+template <int D, bool kDK>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout,
+                    const float* __restrict__ lse, const float* __restrict__ delta,
+                    __bf16* __restrict__ dk_chunks, __bf16* __restrict__ dk_anchor, int heads,
+                    float c_log2, float scale, PackedPlan plan, KeyUnits ku) {
+  using C = Cfg<D>;
+  __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
+  __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
+  const int nq = plan.chunk_tokens, G = plan.frame_tokens;
+  const int n_units = plan.n_chunks * ku.kpc + ku.n_frames * ku.kpf;
+  const int logical = xcd_logical(blockIdx.x, gridDim.x);
+  const int head = logical / n_units;
+  const int unit = logical - head * n_units;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l32 = lane & 31, half = lane >> 5;
+  const int64_t row_elems = int64_t(heads) * D;
+  const bool is_chunk = unit < plan.n_chunks * ku.kpc;
+  int owner, k_first, n_keys;
+  const __bf16 *kbase, *vbase;
+  __bf16* obase;
+  if (is_chunk) {
+    owner = unit / ku.kpc;
+    k_first = (unit % ku.kpc) * kBlockN;
+    n_keys = nq;
+    kbase = static_cast<const __bf16*>(plan.k) + int64_t(owner) * nq * row_elems;
+    vbase = static_cast<const __bf16*>(plan.v) + int64_t(owner) * nq * row_elems;
+    obase = dk_chunks + int64_t(owner) * nq * row_elems;
+  } else {
+    const int a = unit - plan.n_chunks * ku.kpc;
+    owner = a / ku.kpf;
+    k_first = (a % ku.kpf) * kBlockN;
+    n_keys = G;
+    kbase = static_cast<const __bf16*>(plan.ak) + int64_t(owner) * G * row_elems;
+    vbase = static_cast<const __bf16*>(plan.av) + int64_t(owner) * G * row_elems;
+    obase = dk_anchor + int64_t(owner) * G * row_elems;
+  }
+  const int k0 = k_first + wave * 32;
+  bf16x8 kreg[C::KS], vreg[C::KS];
+  load_b<D>(kbase + head * D, row_elems, k0, n_keys, lane, kreg);
+  if constexpr (kDK) load_b<D>(vbase + head * D, row_elems, k0, n_keys, lane, vreg);
+  f32x16 acc[C::DB];
+#pragma unroll
+  for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[db][j] = 0.0f;
+
+  // query runs of this unit
+  Stream<D, true> st;
+  st.wave = wave;
+  st.lane = lane;
+  st.row_bytes = uint32_t(2 * row_elems);
+  st.vec_bytes = uint32_t(4 * heads);
+  auto set_run = [&](int i, int c0, int c1) {   // chunks c0 .. c1 - 1
+    if (lane == i) {
+      const int64_t t0 = int64_t(c0) * nq;
+      st.len = (c1 - c0) * nq;
+      st.a = reinterpret_cast<uint64_t>(q + t0 * row_elems + head * D);
+      st.b = reinterpret_cast<uint64_t>(dout + t0 * row_elems + head * D);
+      st.va = reinterpret_cast<uint64_t>(lse + t0 * heads + head);
+      st.vb = reinterpret_cast<uint64_t>(delta + t0 * heads + head);
+    }
+  };
+  if (is_chunk) {
+    set_run(0, owner, min(owner + plan.window + 1, plan.n_chunks));
+    st.n_runs = 1;
+  } else {
+    int n = 0;
+    while (n < 8 && ku.frame_runs[owner][2 * n + 1] != 0) {
+      const int c0 = ku.frame_runs[owner][2 * n];
+      set_run(n, c0, c0 + ku.frame_runs[owner][2 * n + 1]);
+      ++n;
+    }
+    st.n_runs = n;
+  }
+  st.n_tiles = 0;
+  for (int i = 0; i < st.n_runs; ++i) st.n_tiles += (st.run_len(i) + kBT - 1) / kBT;
+#pragma unroll
+  for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
+    const int r = (wave * C::BLOCKS_PER_WAVE + i) * C::RPB + lane / C::CPR;
+    st.cp_row[i] = r;
+    st.cp_choff[i] = 16 * ((lane % C::CPR) ^ swz<D>(r));
+  }
+  Lanes<D> ln(lane);
+  int csg = 0, ck0 = 0;
+
+  auto tile = [&](int t, char* cur, char* nxt) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (t + 1 < st.n_tiles) st.issue(nxt);
+    // keep the per-read address arithmetic inside the loop (no hoisted copies)
+    asm volatile("" : "+v"(ln.a_lane), "+v"(ln.t_lane[0]), "+v"(ln.t_lane[1]));
+    const int nv = min(kBT, st.run_len(csg) - ck0);
+    const float* lse_t = reinterpret_cast<const float*>(cur + 2 * C::TILE);
+    const float* del_t = reinterpret_cast<const float*>(cur + 2 * C::TILE + C::VEC);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 s;
+      rows_times_b<D>(cur, kb, ln.a_lane, kreg, s);               // S = Q K^T (rows = queries)
+      __builtin_amdgcn_sched_barrier(0);
+      f32x16 dp;
+      if constexpr (kDK) rows_times_b<D>(cur + C::TILE, kb, ln.a_lane, vreg, dp);   // dP = dO V^T
+      __builtin_amdgcn_sched_barrier(0);
+      uint32_t pk[8];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int r0 = kb * 32 + 8 * g + 4 * half;
+        const f32x4 Lr = *reinterpret_cast<const f32x4*>(lse_t + r0);
+        f32x4 Dr;
+        if constexpr (kDK) Dr = *reinterpret_cast<const f32x4*>(del_t + r0);
+        float v4[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float p = r0 + e < nv ? __builtin_amdgcn_exp2f(fmaf(s[4 * g + e], c_log2, -Lr[e])) : 0.0f;
+          if constexpr (kDK) v4[e] = p * (dp[4 * g + e] - Dr[e]);
+          else v4[e] = p;
+        }
+        pk[2 * g] = pack_bf16(v4[0], v4[1]);
+        pk[2 * g + 1] = pack_bf16(v4[2], v4[3]);
+      }
+      // dV^T += dO^T P, dK^T += Q^T dS
+      rows_t_times_p<D>(kDK ? cur : cur + C::TILE, kb, ln.t_lane, pk, acc);
+      __builtin_amdgcn_sched_barrier(0);   // one 32-query block at a time (register budget)
+    }
+    st.advance(csg, ck0);
+  };
+  if (st.n_tiles > 0) st.issue(lds0);
+  for (int t = 0; t < st.n_tiles;) {
+    tile(t, lds0, lds1);
+    if (++t >= st.n_tiles) break;
+    tile(t, lds1, lds0);
+    ++t;
+  }
+  store_t<D>(obase + head * D, row_elems, k0 + l32, n_keys, lane, acc, kDK ? scale : 1.0f);
+}
+
+}  // namespace
+
+hipError_t launch_attention_bwd_bf16(const void* q, const void* out, const void* dout,
+                                     const float* lse, float* delta, void* dq, void* dk, void* dv,
+                                     void* dak, void* dav, int heads, int head_dim,
+                                     float softmax_scale, const PackedPlan& plan,
+                                     const uint8_t (*frame_runs)[16], int n_frames,
+                                     hipStream_t stream) {
+  const int nq = plan.chunk_tokens;
+  const int64_t rows = int64_t(plan.n_chunks) * nq * heads;
+  if (rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(bwd_delta_kernel, dim3(unsigned((rows + 255) / 256)), dim3(256), 0, stream,
+                     static_cast<const __bf16*>(out), static_cast<const __bf16*>(dout), delta, rows,
+                     head_dim);
+  const float c_log2 = float(double(softmax_scale) * 1.4426950408889634);
+  const int n_qtiles = (nq + kBlockN - 1) / kBlockN;
+  KeyUnits ku;
+  std::memset(&ku, 0, sizeof(ku));
+  ku.kpc = n_qtiles;
+  ku.kpf = (plan.frame_tokens + kBlockN - 1) / kBlockN;
+  ku.n_frames = n_frames;
+  for (int f = 0; f < n_frames; ++f) std::memcpy(ku.frame_runs[f], frame_runs[f], 16);
+  const int n_units = plan.n_chunks * ku.kpc + n_frames * ku.kpf;
+  const dim3 g_q(unsigned(plan.n_chunks * heads * n_qtiles)), g_k(unsigned(n_units * heads));
+  const __bf16* qp = static_cast<const __bf16*>(q);
+  const __bf16* dp = static_cast<const __bf16*>(dout);
+  if (head_dim == 128) {
+    hipLaunchKernelGGL(bwd_dq_kernel<128>, g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
+                       static_cast<__bf16*>(dq), heads, c_log2, softmax_scale, plan, n_qtiles);
+    hipLaunchKernelGGL((bwd_dkv_kernel<128, false>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+                       delta, static_cast<__bf16*>(dv), static_cast<__bf16*>(dav), heads, c_log2,
+                       softmax_scale, plan, ku);
+    hipLaunchKernelGGL((bwd_dkv_kernel<128, true>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+                       delta, static_cast<__bf16*>(dk), static_cast<__bf16*>(dak), heads, c_log2,
+                       softmax_scale, plan, ku);
+  } else {
+    hipLaunchKernelGGL(bwd_dq_kernel<64>, g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
+                       static_cast<__bf16*>(dq), heads, c_log2, softmax_scale, plan, n_qtiles);
+    hipLaunchKernelGGL((bwd_dkv_kernel<64, false>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+                       delta, static_cast<__bf16*>(dv), static_cast<__bf16*>(dav), heads, c_log2,
+                       softmax_scale, plan, ku);
+    hipLaunchKernelGGL((bwd_dkv_kernel<64, true>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+                       delta, static_cast<__bf16*>(dk), static_cast<__bf16*>(dak), heads, c_log2,
+                       softmax_scale, plan, ku);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ff

@@ -11,6 +11,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <climits>
 #include <cmath>
 #include <cstdarg>
@@ -451,9 +452,12 @@ ff_status ff_cache_read(const ff_cache* cache, int32_t stage, int32_t layer, int
   return hip_status(e, "cache_read launch");
 }
 
-ff_status ff_packed_attention(const ff_packed_desc* desc, const void* q, const void* k,
-                              const void* v, const void* anchor_k, const void* anchor_v,
-                              void* out, float softmax_scale, void* stream) {
+namespace {
+
+// Validate a packed launch and fill its plan (anchor frames grouped into runs).
+ff_status make_packed_plan(const ff_packed_desc* desc, const void* q, const void* k, const void* v,
+                           const void* anchor_k, const void* anchor_v, const void* out,
+                           float softmax_scale, ff::PackedPlan* plan) {
   if (!desc) return fail(FF_ERR_INVALID_ARG, "desc is NULL");
   const ff_packed_desc& d = *desc;
   if (d.n_chunks < 1 || d.n_chunks > FF_MAX_PACKED_CHUNKS)
@@ -486,16 +490,16 @@ ff_status ff_packed_attention(const ff_packed_desc* desc, const void* q, const v
     return fail(FF_ERR_UNSUPPORTED, "a chunk window of %lld tokens spans more than 4 GiB",
                 (long long)window_tokens);
 
-  ff::PackedPlan plan;
-  std::memset(&plan, 0, sizeof(plan));
-  plan.k = k;
-  plan.v = v;
-  plan.ak = anchor_k;
-  plan.av = anchor_v;
-  plan.chunk_tokens = d.chunk_tokens;
-  plan.frame_tokens = d.frame_tokens;
-  plan.window = d.window;
-  plan.n_chunks = d.n_chunks;
+  ff::PackedPlan& plan_ = *plan;
+  std::memset(&plan_, 0, sizeof(plan_));
+  plan_.k = k;
+  plan_.v = v;
+  plan_.ak = anchor_k;
+  plan_.av = anchor_v;
+  plan_.chunk_tokens = d.chunk_tokens;
+  plan_.frame_tokens = d.frame_tokens;
+  plan_.window = d.window;
+  plan_.n_chunks = d.n_chunks;
   for (int c = 0; c < d.n_chunks && d.n_anchor_frames > 0; ++c) {
     bool seen[256] = {false};
     for (int j = 0; j < FF_MAX_ANCHOR_FRAMES; ++j) {
@@ -514,12 +518,29 @@ ff_status ff_packed_attention(const ff_packed_desc* desc, const void* q, const v
       while (e < d.n_anchor_frames && seen[e]) ++e;
       if (int64_t(e - f) * d.frame_tokens * row > int64_t(UINT32_MAX))
         return fail(FF_ERR_UNSUPPORTED, "anchor frames %d .. %d span more than 4 GiB", f, e - 1);
-      plan.runs[c][2 * n_runs] = uint8_t(f);
-      plan.runs[c][2 * n_runs + 1] = uint8_t(e - f);
+      plan_.runs[c][2 * n_runs] = uint8_t(f);
+      plan_.runs[c][2 * n_runs + 1] = uint8_t(e - f);
       ++n_runs;
       f = e;
     }
   }
+  return FF_OK;
+}
+
+}  // namespace
+
+ff_status ff_packed_attention(const ff_packed_desc* desc, const void* q, const void* k,
+                              const void* v, const void* anchor_k, const void* anchor_v,
+                              void* out, float softmax_scale, float* lse, void* stream) {
+  ff::PackedPlan plan;
+  ff_status st = make_packed_plan(desc, q, k, v, anchor_k, anchor_v, out, softmax_scale, &plan);
+  if (st != FF_OK) return st;
+  const ff_packed_desc& d = *desc;
+  if (lse) {
+    if (d.dtype != FF_DT_BF16) return fail(FF_ERR_UNSUPPORTED, "lse is produced by the bf16 path");
+    if (reinterpret_cast<uintptr_t>(lse) % 4 != 0) return fail(FF_ERR_INVALID_ARG, "lse misaligned");
+  }
+  plan.lse = lse;
   hipError_t e;
   if (d.dtype == FF_DT_BF16)
     e = ff::launch_attention_bf16_packed(q, out, d.num_heads, d.head_dim, softmax_scale, plan,
@@ -528,6 +549,73 @@ ff_status ff_packed_attention(const ff_packed_desc* desc, const void* q, const v
     e = ff::launch_attention_f32_packed(q, out, d.num_heads, d.head_dim, softmax_scale, plan,
                                         static_cast<hipStream_t>(stream));
   return hip_status(e, "packed_attention launch");
+}
+
+size_t ff_packed_attention_bwd_workspace(const ff_packed_desc* desc) {
+  if (!desc || desc->n_chunks < 1 || desc->chunk_tokens < 1 || desc->num_heads < 1) return 0;
+  return size_t(desc->n_chunks) * desc->chunk_tokens * desc->num_heads * sizeof(float);
+}
+
+ff_status ff_packed_attention_bwd(const ff_packed_desc* desc, const void* q, const void* k,
+                                  const void* v, const void* anchor_k, const void* anchor_v,
+                                  const void* out, const void* dout, const float* lse, void* dq,
+                                  void* dk, void* dv, void* d_anchor_k, void* d_anchor_v,
+                                  float softmax_scale, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  ff::PackedPlan plan;
+  ff_status st = make_packed_plan(desc, q, k, v, anchor_k, anchor_v, out, softmax_scale, &plan);
+  if (st != FF_OK) return st;
+  const ff_packed_desc& d = *desc;
+  if (d.dtype != FF_DT_BF16) return fail(FF_ERR_UNSUPPORTED, "the backward pass is bf16 only");
+  if (d.n_anchor_frames > 64)
+    return fail(FF_ERR_UNSUPPORTED, "the backward pass takes at most 64 anchor frames");
+  if (!dout || !lse || !dq || !dk || !dv || !workspace)
+    return fail(FF_ERR_INVALID_ARG, "dout, lse, dq, dk, dv and workspace must be non-NULL");
+  if (d.n_anchor_frames > 0 && (!d_anchor_k || !d_anchor_v))
+    return fail(FF_ERR_INVALID_ARG, "d_anchor_k / d_anchor_v must be non-NULL with anchor frames");
+  if (check_aligned(dout, "dout") != FF_OK || check_aligned(dq, "dq") != FF_OK ||
+      check_aligned(dk, "dk") != FF_OK || check_aligned(dv, "dv") != FF_OK ||
+      check_aligned(workspace, "workspace") != FF_OK ||
+      (d.n_anchor_frames > 0 && (check_aligned(d_anchor_k, "d_anchor_k") != FF_OK ||
+                                 check_aligned(d_anchor_v, "d_anchor_v") != FF_OK)))
+    return FF_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(lse) % 4 != 0) return fail(FF_ERR_INVALID_ARG, "lse misaligned");
+  const size_t need = ff_packed_attention_bwd_workspace(desc);
+  if (workspace_bytes < need)
+    return fail(FF_ERR_BUFFER, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  // chunks that see each anchor frame, as runs of consecutive chunks
+  std::vector<std::array<uint8_t, 16>> frame_runs(std::max(d.n_anchor_frames, 1));
+  for (int f = 0; f < d.n_anchor_frames; ++f) {
+    std::fill(frame_runs[f].begin(), frame_runs[f].end(), uint8_t(0));
+    int n = 0;
+    for (int c = 0; c < d.n_chunks;) {
+      bool sees = false;
+      for (int j = 0; j < FF_MAX_ANCHOR_FRAMES; ++j)
+        sees |= d.anchors_of_chunk[c * FF_MAX_ANCHOR_FRAMES + j] == f;
+      if (!sees) { ++c; continue; }
+      int e = c + 1;
+      for (; e < d.n_chunks; ++e) {
+        bool s2 = false;
+        for (int j = 0; j < FF_MAX_ANCHOR_FRAMES; ++j)
+          s2 |= d.anchors_of_chunk[e * FF_MAX_ANCHOR_FRAMES + j] == f;
+        if (!s2) break;
+      }
+      if (n == 8)
+        return fail(FF_ERR_UNSUPPORTED, "anchor frame %d is seen by more than 8 runs of chunks", f);
+      if (int64_t(e - c) * d.chunk_tokens * 2 * d.num_heads * d.head_dim > int64_t(UINT32_MAX))
+        return fail(FF_ERR_UNSUPPORTED, "a run of chunks spans more than 4 GiB");
+      frame_runs[f][2 * n] = uint8_t(c);
+      frame_runs[f][2 * n + 1] = uint8_t(e - c);
+      ++n;
+      c = e;
+    }
+  }
+  hipError_t e = ff::launch_attention_bwd_bf16(
+      q, out, dout, lse, static_cast<float*>(workspace), dq, dk, dv, d_anchor_k, d_anchor_v,
+      d.num_heads, d.head_dim, softmax_scale, plan,
+      reinterpret_cast<const uint8_t(*)[16]>(frame_runs.data()), d.n_anchor_frames,
+      static_cast<hipStream_t>(stream));
+  return hip_status(e, "packed_attention_bwd launch");
 }
 
 ff_status ff_anchor_partition(int32_t L, int32_t delta, int32_t* out, int32_t capacity,

@@ -43,6 +43,7 @@ struct PackedPlan {
   const void* v;
   const void* ak;           // [n_frames * frame_tokens][heads][d]
   const void* av;
+  float* lse;               // optional [n_chunks * chunk_tokens][heads]: base-2 log-sum-exp
   int32_t chunk_tokens;
   int32_t frame_tokens;
   int32_t window;
@@ -118,6 +119,16 @@ hipError_t launch_attention_bf16_packed(const void* q, void* out, int heads, int
 hipError_t launch_attention_f32_packed(const void* q, void* out, int heads, int head_dim,
                                        float softmax_scale, const PackedPlan& plan,
                                        hipStream_t stream);
+
+// Backward pass of a packed launch (bf16): delta (workspace, [rows][heads]
+// f32) = dO . O, then dQ, dV and dK; frame_runs[f] lists the (first chunk,
+// count) runs of chunks that see anchor frame f.
+hipError_t launch_attention_bwd_bf16(const void* q, const void* out, const void* dout,
+                                     const float* lse, float* delta, void* dq, void* dk, void* dv,
+                                     void* dak, void* dav, int heads, int head_dim,
+                                     float softmax_scale, const PackedPlan& plan,
+                                     const uint8_t (*frame_runs)[16], int n_frames,
+                                     hipStream_t stream);
 
 // Euler step x_out = x - dsigma * v over n elements of dtype (x_out may be x).
 hipError_t launch_euler(const void* x, const void* v, void* y, int64_t n, double dsigma,

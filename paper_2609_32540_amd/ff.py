@@ -81,7 +81,11 @@ SIGNATURES = [
     ("ff_cache_anchor_state", _I32, [_VP, _I32, _PI32, _PI32]),
     ("ff_cache_read", _I32, [_VP, _I32, _I32, _I32, _VP, _VP, _VP]),
     ("ff_packed_attention", _I32, [ctypes.POINTER(PackedDesc), _VP, _VP, _VP, _VP, _VP, _VP,
-                                   ctypes.c_float, _VP]),
+                                   ctypes.c_float, _VP, _VP]),
+    ("ff_packed_attention_bwd_workspace", _SZ, [ctypes.POINTER(PackedDesc)]),
+    ("ff_packed_attention_bwd", _I32, [ctypes.POINTER(PackedDesc), _VP, _VP, _VP, _VP, _VP, _VP,
+                                       _VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_float, _VP,
+                                       _SZ, _VP]),
     ("ff_anchor_partition", _I32, [_I32, _I32, _PI32, _I32, _PI32]),
     ("ff_anchor_window", _I32, [_I64, _I32, _I32, _I32, _PI32, _PI32]),
     ("ff_euler_step", _I32, [_VP, _VP, _VP, _I64, ctypes.c_double, _I32, _VP]),
@@ -294,32 +298,13 @@ def _dense(t: torch.Tensor, shape: Tuple[int, ...], dtype: torch.dtype, device: 
     return t.data_ptr()
 
 
-def packed_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, *, n_chunks: int,
-                     window: int, anchor_k: Optional[torch.Tensor] = None,
-                     anchor_v: Optional[torch.Tensor] = None, frame_tokens: int = 0,
-                     anchors_of_chunk: Optional[Sequence[Sequence[int]]] = None,
-                     out: Optional[torch.Tensor] = None, scale: Optional[float] = None,
-                     stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
-    """ff_packed_attention: every chunk of one stage in one launch.
-
-    q, k, v: [n_chunks * chunk_tokens][heads][d]; anchor_k / anchor_v:
-    [n_frames * frame_tokens][heads][d]; anchors_of_chunk[i] lists the anchor
-    frame indices chunk i sees.
-    """
+def _packed_desc(q, n_chunks, window, anchor_k, anchor_v, frame_tokens, anchors_of_chunk):
     if q.dim() != 3 or q.shape[0] % n_chunks:
         raise ValueError("q must be [n_chunks * chunk_tokens][heads][d]")
     chunk_tokens = q.shape[0] // n_chunks
     heads, d = q.shape[1], q.shape[2]
-    dev, dt = q.device, q.dtype
-    if dt not in (torch.bfloat16, torch.float32):
+    if q.dtype not in (torch.bfloat16, torch.float32):
         raise ValueError("dtype must be torch.bfloat16 or torch.float32")
-    shape = (n_chunks * chunk_tokens, heads, d)
-    qp = _dense(q, shape, dt, dev, "q")
-    kp = _dense(k, shape, dt, dev, "k")
-    vp = _dense(v, shape, dt, dev, "v")
-    if out is None:
-        out = torch.empty_like(q)
-    op = _dense(out, shape, dt, dev, "out")
     n_frames = 0
     akp = avp = None
     table = None
@@ -328,8 +313,8 @@ def packed_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, *, n_chu
             raise ValueError("anchor_k must hold whole frames of frame_tokens tokens")
         n_frames = anchor_k.shape[0] // frame_tokens
         a_shape = (n_frames * frame_tokens, heads, d)
-        akp = _dense(anchor_k, a_shape, dt, dev, "anchor_k")
-        avp = _dense(anchor_v, a_shape, dt, dev, "anchor_v")
+        akp = _dense(anchor_k, a_shape, q.dtype, q.device, "anchor_k")
+        avp = _dense(anchor_v, a_shape, q.dtype, q.device, "anchor_v")
         flat = [-1] * (n_chunks * MAX_ANCHOR_FRAMES)
         for i, frames in enumerate(anchors_of_chunk or []):
             if len(frames) > MAX_ANCHOR_FRAMES:
@@ -338,13 +323,66 @@ def packed_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, *, n_chu
                 flat[i * MAX_ANCHOR_FRAMES + j] = int(f)
         table = (ctypes.c_int32 * len(flat))(*flat)
     desc = PackedDesc(n_chunks, chunk_tokens, heads, d, window, frame_tokens, n_frames,
-                      FF_DT_BF16 if dt == torch.bfloat16 else FF_DT_F32,
+                      FF_DT_BF16 if q.dtype == torch.bfloat16 else FF_DT_F32,
                       ctypes.cast(table, ctypes.POINTER(ctypes.c_int32)) if table is not None else None)
+    return desc, table, akp, avp, (n_chunks * chunk_tokens, heads, d), n_frames
+
+
+def packed_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, *, n_chunks: int,
+                     window: int, anchor_k: Optional[torch.Tensor] = None,
+                     anchor_v: Optional[torch.Tensor] = None, frame_tokens: int = 0,
+                     anchors_of_chunk: Optional[Sequence[Sequence[int]]] = None,
+                     out: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+                     lse: Optional[torch.Tensor] = None,
+                     stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """ff_packed_attention: every chunk of one stage in one launch.
+
+    q, k, v: [n_chunks * chunk_tokens][heads][d]; anchor_k / anchor_v:
+    [n_frames * frame_tokens][heads][d]; anchors_of_chunk[i] lists the anchor
+    frame indices chunk i sees.  lse (optional, float32 [tokens][heads])
+    receives the base-2 log-sum-exp the backward pass needs.
+    """
+    desc, table, akp, avp, shape, _ = _packed_desc(q, n_chunks, window, anchor_k, anchor_v,
+                                                   frame_tokens, anchors_of_chunk)
+    dev, dt = q.device, q.dtype
+    qp = _dense(q, shape, dt, dev, "q")
+    kp = _dense(k, shape, dt, dev, "k")
+    vp = _dense(v, shape, dt, dev, "v")
+    if out is None:
+        out = torch.empty_like(q)
+    op = _dense(out, shape, dt, dev, "out")
+    lp = _dense(lse, shape[:2], torch.float32, dev, "lse") if lse is not None else None
     if scale is None:
-        scale = 1.0 / math.sqrt(d)
+        scale = 1.0 / math.sqrt(shape[2])
     _check(lib().ff_packed_attention(ctypes.byref(desc), qp, kp, vp, akp, avp, op,
-                                     ctypes.c_float(scale), _stream_handle(dev, stream)))
+                                     ctypes.c_float(scale), lp, _stream_handle(dev, stream)))
     return out
+
+
+def packed_attention_bwd(q, k, v, out, dout, lse, *, n_chunks: int, window: int,
+                         anchor_k=None, anchor_v=None, frame_tokens: int = 0,
+                         anchors_of_chunk=None, scale: Optional[float] = None,
+                         stream: Optional[torch.cuda.Stream] = None):
+    """ff_packed_attention_bwd: returns (dq, dk, dv, d_anchor_k, d_anchor_v)."""
+    desc, table, akp, avp, shape, n_frames = _packed_desc(q, n_chunks, window, anchor_k, anchor_v,
+                                                          frame_tokens, anchors_of_chunk)
+    dev, dt = q.device, q.dtype
+    ptrs = [_dense(t, shape, dt, dev, n) for t, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out"),
+                                                      (dout, "dout"))]
+    lp = _dense(lse, shape[:2], torch.float32, dev, "lse")
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    dak = torch.empty_like(anchor_k) if anchor_k is not None else None
+    dav = torch.empty_like(anchor_v) if anchor_v is not None else None
+    ws_bytes = lib().ff_packed_attention_bwd_workspace(ctypes.byref(desc))
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
+    if scale is None:
+        scale = 1.0 / math.sqrt(shape[2])
+    _check(lib().ff_packed_attention_bwd(
+        ctypes.byref(desc), ptrs[0], ptrs[1], ptrs[2], akp, avp, ptrs[3], ptrs[4], lp,
+        dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+        dak.data_ptr() if dak is not None else None, dav.data_ptr() if dav is not None else None,
+        ctypes.c_float(scale), ws.data_ptr(), ws.numel(), _stream_handle(dev, stream)))
+    return dq, dk, dv, dak, dav
 
 
 def anchor_partition(L: int, delta: int) -> List[int]:

@@ -34,7 +34,7 @@ def desc(**kw):
 def test_library_exports_every_header_symbol():
     L = ff.lib()
     names = header_functions()
-    assert len(names) == 19
+    assert len(names) == 21
     for n in names:
         assert hasattr(L, n), n
     assert {n for n, _, _ in ff.SIGNATURES} == set(names)
@@ -147,7 +147,7 @@ def packed_desc(**kw):
 def packed_call(d, q=FAKE_DEV, k=FAKE_DEV, v=FAKE_DEV, ak=None, av=None, out=FAKE_DEV, scale=0.125):
     L = ff.lib()
     return L.ff_packed_attention(ctypes.byref(d) if d is not None else None, q, k, v, ak, av, out,
-                                 ctypes.c_float(scale), None)
+                                 ctypes.c_float(scale), None, None)
 
 
 def table(rows):

@@ -1,0 +1,163 @@
+"""GPU parity of the packed attention backward (ff_packed_attention_bwd) and
+of the forward's log-sum-exp against the float64 oracle gradient of the
+packed block-causal mask.  Bar (bf16 operands P and dS, float32 accumulation,
+gradients rounded to bf16): relative-L2 <= 1e-2 per gradient tensor and
+max-abs <= 3e-2 of the tensor's largest magnitude; log-sum-exp within 2e-3
+(log2 units)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import ff_oracle as fo
+from paper_2609_32540_amd import ff
+
+from gpu_util import exact, rel_l2, to_dev
+
+pytestmark = pytest.mark.gpu
+
+GRAD_REL_L2 = 1e-2
+GRAD_MAX_REL = 3e-2
+LSE_ABS = 2e-3
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _needs_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ff.lib()
+
+
+def check_grad(got, ref, what):
+    got = got.astype(np.float64)
+    assert np.isfinite(got).all(), what
+    rl = rel_l2(got, ref)
+    mx = float(np.abs(got - ref).max())
+    big = float(np.abs(ref).max())
+    assert rl <= GRAD_REL_L2 and mx <= GRAD_MAX_REL * big, f"{what}: rel-L2 {rl:.2e}, max-abs {mx:.2e} (max |ref| {big:.2e})"
+    return rl
+
+
+def run_case(n, Nq, G, n_frames, table, W, heads, d, seed=0, hidden_frame=False):
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+
+    def rnd(shape, s=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * s).to(torch.bfloat16)
+    q, k, v = rnd((n * Nq, heads, d)), rnd((n * Nq, heads, d)), rnd((n * Nq, heads, d))
+    ak, av = rnd((n_frames * G, heads, d)), rnd((n_frames * G, heads, d))
+    dout = rnd((n * Nq, heads, d))
+    scale = 1.0 / math.sqrt(d)
+    lse = torch.empty((n * Nq, heads), dtype=torch.float32, device=dev)
+    out = ff.packed_attention(q, k, v, n_chunks=n, window=W, anchor_k=ak, anchor_v=av,
+                              frame_tokens=G, anchors_of_chunk=table, scale=scale, lse=lse)
+    dq, dk, dv, dak, dav = ff.packed_attention_bwd(q, k, v, out, dout, lse, n_chunks=n, window=W,
+                                                   anchor_k=ak, anchor_v=av, frame_tokens=G,
+                                                   anchors_of_chunk=table, scale=scale)
+    torch.cuda.synchronize()
+    # oracle over the packed sequence [anchor frames | chunks]
+    M = fo.packed_visibility(n, Nq, G, n_frames, table, W)
+    K_all = np.concatenate([exact(ak), exact(k)])
+    V_all = np.concatenate([exact(av), exact(v)])
+    rdq, rdk, rdv = fo.masked_attention_grad(exact(q), K_all, V_all, M, exact(dout), scale)
+    rlse = fo.log2_sum_exp2(exact(q), K_all, M, scale)
+    assert float(np.abs(exact(lse) - rlse).max()) <= LSE_ABS
+    na = n_frames * G
+    check_grad(exact(dq), rdq, "dq")
+    check_grad(exact(dk), rdk[na:], "dk")
+    check_grad(exact(dv), rdv[na:], "dv")
+    seen = M[:, :na].any(axis=0)
+    if seen.any():
+        check_grad(exact(dak)[seen], rdk[:na][seen], "d_anchor_k")
+        check_grad(exact(dav)[seen], rdv[:na][seen], "d_anchor_v")
+    if hidden_frame:
+        assert not seen.all()
+        assert (exact(dak)[~seen] == 0).all() and (exact(dav)[~seen] == 0).all()
+
+
+TABLE6 = [[], [2, 0], [0, 1, 2], [1], [2, 1], [0, 2]]
+
+
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("W", [0, 2, 9])
+def test_backward_small(d, W):
+    run_case(6, 198, 66, 3, TABLE6, W, 2, d)
+
+
+def test_backward_multi_tile_and_hidden_frame():
+    # 288-token chunks (4.5 tiles), 96-token frames, a frame no chunk lists, 4 heads
+    table = [[0], [0, 1], [1], [1, 3], [3], [3]]
+    run_case(6, 288, 96, 4, table, 3, 4, 128, seed=3, hidden_frame=True)
+
+
+def test_backward_frame_seen_by_several_chunk_runs():
+    # frame 0 is seen by chunks {0, 1, 3, 5}: three runs of consecutive chunks
+    table = [[0], [0], [1], [0, 1], [1], [0]]
+    run_case(6, 130, 64, 2, table, 1, 2, 128, seed=5)
+
+
+def test_backward_full_clip_sampled():
+    """1.3B 480p clip (27 chunks x 4680 tokens, 12 heads x 128, W = 4, Gamma(i)
+    windows from a 9-frame bank): one backward; dQ of sampled query rows and
+    dK, dV of sampled keys of a chunk against float64 over their visible sets."""
+    w = synth.WORKLOADS["1.3b-480p"]
+    n, W, Nq, G, h, d = w.n_chunks, w.ring_chunks, w.chunk_tokens, w.tokens_per_frame, w.heads, w.head_dim
+    dev = torch.device("cuda", 0)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(9)
+    rnd = lambda shape: torch.randn(shape, generator=gen, device=dev).to(torch.bfloat16)
+    q, k, v, dout = (rnd((n * Nq, h, d)) for _ in range(4))
+    frames = sorted({f for c in range(n) for f in w.anchor_frames_for_chunk(c)})
+    ak, av = rnd((len(frames) * G, h, d)), rnd((len(frames) * G, h, d))
+    table = [[frames.index(f) for f in w.anchor_frames_for_chunk(c)] for c in range(n)]
+    scale = 1.0 / math.sqrt(d)
+    lse = torch.empty((n * Nq, h), dtype=torch.float32, device=dev)
+    out = ff.packed_attention(q, k, v, n_chunks=n, window=W, anchor_k=ak, anchor_v=av,
+                              frame_tokens=G, anchors_of_chunk=table, scale=scale, lse=lse)
+    dq, dk, dv, dak, dav = ff.packed_attention_bwd(q, k, v, out, dout, lse, n_chunks=n, window=W,
+                                                   anchor_k=ak, anchor_v=av, frame_tokens=G,
+                                                   anchors_of_chunk=table, scale=scale)
+    torch.cuda.synchronize()
+    for t in (dq, dk, dv, dak, dav):
+        assert torch.isfinite(t.float()).all()
+    hd = 5
+    c = 13
+    # dQ rows of chunk c: softmax over its visible keys
+    rows = np.concatenate([np.arange(0, 64), np.arange(Nq - 40, Nq)]) + c * Nq
+    keys_k = np.concatenate([exact(ak[f * G:(f + 1) * G, hd]) for f in table[c]] +
+                            [exact(k[max(0, c - W) * Nq:(c + 1) * Nq, hd])])
+    keys_v = np.concatenate([exact(av[f * G:(f + 1) * G, hd]) for f in table[c]] +
+                            [exact(v[max(0, c - W) * Nq:(c + 1) * Nq, hd])])
+    Qr, dOr = exact(q[rows, hd]).astype(np.float64), exact(dout[rows, hd]).astype(np.float64)
+    s = scale * Qr @ keys_k.T.astype(np.float64)
+    P = np.exp(s - s.max(1, keepdims=True))
+    P /= P.sum(1, keepdims=True)
+    dP = dOr @ keys_v.T.astype(np.float64)
+    dS = P * (dP - (dP * P).sum(1, keepdims=True))
+    check_grad(exact(dq[rows, hd]), scale * dS @ keys_k.astype(np.float64), "dq rows")
+    # dK, dV of keys of chunk c: every query of chunks c .. c + W, each with its own softmax
+    key_rows = np.arange(c * Nq + 100, c * Nq + 164)
+    kk = exact(k[key_rows, hd]).astype(np.float64)
+    vv = exact(v[key_rows, hd]).astype(np.float64)
+    gdk = np.zeros_like(kk)
+    gdv = np.zeros_like(vv)
+    for i in range(c, min(c + W, n - 1) + 1):
+        qi = exact(q[i * Nq:(i + 1) * Nq, hd]).astype(np.float64)
+        doi = exact(dout[i * Nq:(i + 1) * Nq, hd]).astype(np.float64)
+        Ki = np.concatenate([exact(ak[f * G:(f + 1) * G, hd]) for f in table[i]] +
+                            [exact(k[max(0, i - W) * Nq:(i + 1) * Nq, hd])]).astype(np.float64)
+        Vi = np.concatenate([exact(av[f * G:(f + 1) * G, hd]) for f in table[i]] +
+                            [exact(v[max(0, i - W) * Nq:(i + 1) * Nq, hd])]).astype(np.float64)
+        si = scale * qi @ Ki.T
+        Pi = np.exp(si - si.max(1, keepdims=True))
+        Pi /= Pi.sum(1, keepdims=True)
+        Di = ((doi @ Vi.T) * Pi).sum(1, keepdims=True)
+        Pk = np.exp(scale * qi @ kk.T - si.max(1, keepdims=True)) / np.exp(si - si.max(1, keepdims=True)).sum(1, keepdims=True)
+        dPk = doi @ vv.T
+        gdv += Pk.T @ doi
+        gdk += scale * (Pk * (dPk - Di)).T @ qi
+    check_grad(exact(dv[key_rows, hd]), gdv, "dv keys")
+    check_grad(exact(dk[key_rows, hd]), gdk, "dk keys")

@@ -454,3 +454,79 @@ def test_wavefront_schedule_rounds_and_coverage(N_R, S):
     total, _, _ = fo.forward_counts(L, 10, B, S)
     M = len(fo.anchor_partition(L, 10))
     assert total - fo.num_blocks(M, B) * (S + 1) == N_R * S
+
+
+# --------------------------------------------------------------------------
+# attention backward (packed training forward)
+
+def _packed_case(seed=0, n=3, Nq=5, G=4, nf=2, h=2, d=8, W=1):
+    rng = np.random.default_rng(seed)
+    table = [[0], [1, 0], [1]][:n]
+    M = fo.packed_visibility(n, Nq, G, nf, table, W)
+    Q = rng.standard_normal((n * Nq, h, d))
+    K = rng.standard_normal((nf * G + n * Nq, h, d))
+    V = rng.standard_normal((nf * G + n * Nq, h, d))
+    dO = rng.standard_normal((n * Nq, h, d))
+    return Q, K, V, dO, M
+
+
+def test_packed_visibility_rows():
+    M = fo.packed_visibility(3, 2, 1, 2, [[0], [], [0, 1]], 1)
+    assert M.shape == (6, 2 + 6)
+    np.testing.assert_array_equal(M[0], [1, 0, 1, 1, 0, 0, 0, 0])
+    np.testing.assert_array_equal(M[2], [0, 0, 1, 1, 1, 1, 0, 0])
+    np.testing.assert_array_equal(M[5], [1, 1, 0, 0, 1, 1, 1, 1])
+
+
+def test_attention_grad_matches_autograd():
+    Q, K, V, dO, M = _packed_case(nf=3)          # anchor frame 2 is listed for no chunk
+    scale = 0.35
+    dQ, dK, dV = fo.masked_attention_grad(Q, K, V, M, dO, scale)
+    tQ, tK, tV = (torch.tensor(a, dtype=torch.float64, requires_grad=True) for a in (Q, K, V))
+    mask = torch.tensor(M)
+    outs = []
+    for h in range(Q.shape[1]):
+        s = scale * tQ[:, h] @ tK[:, h].T
+        s = s.masked_fill(~mask, float("-inf"))
+        outs.append(torch.softmax(s, dim=-1) @ tV[:, h])
+    out = torch.stack(outs, 1)
+    out.backward(torch.tensor(dO))
+    np.testing.assert_allclose(dQ, tQ.grad.numpy(), atol=1e-12)
+    np.testing.assert_allclose(dK, tK.grad.numpy(), atol=1e-12)
+    np.testing.assert_allclose(dV, tV.grad.numpy(), atol=1e-12)
+    # keys no query sees get no gradient
+    hidden = ~M.any(axis=0)
+    assert hidden.any()
+    assert np.all(dK[hidden] == 0) and np.all(dV[hidden] == 0)
+
+
+def test_attention_grad_finite_differences():
+    Q, K, V, dO, M = _packed_case(seed=4, n=2, Nq=3, G=2, nf=2, h=1, d=4)
+    scale = 0.5
+
+    def loss(Q, K, V):
+        # forward row by row with the oracle's masked attention (one visibility row each)
+        O = np.concatenate([fo.masked_attention(Q[r:r + 1], K, V, M[r], scale)
+                            for r in range(Q.shape[0])])
+        return float((O * dO).sum())
+    dQ, dK, dV = fo.masked_attention_grad(Q, K, V, M, dO, scale)
+    eps = 1e-6
+    for arr, grad in ((Q, dQ), (K, dK), (V, dV)):
+        for idx in [(0, 0, 1), (arr.shape[0] - 1, 0, 3), (arr.shape[0] // 2, 0, 0)]:
+            a1, a2 = arr.copy(), arr.copy()
+            a1[idx] += eps
+            a2[idx] -= eps
+            args1 = [a1 if arr is x else x for x in (Q, K, V)]
+            args2 = [a2 if arr is x else x for x in (Q, K, V)]
+            num = (loss(*args1) - loss(*args2)) / (2 * eps)
+            assert abs(num - grad[idx]) < 1e-6 * max(1.0, abs(num)), (idx, num, grad[idx])
+
+
+def test_log2_sum_exp2_recovers_softmax():
+    Q, K, V, dO, M = _packed_case(seed=2)
+    scale = 0.3
+    lse2 = fo.log2_sum_exp2(Q, K, M, scale)
+    for h in range(Q.shape[1]):
+        s = scale * np.log2(np.e) * (Q[:, h] @ K[:, h].T)
+        P = np.where(M, np.exp2(s - lse2[:, h:h + 1]), 0.0)
+        np.testing.assert_allclose(P.sum(axis=1), 1.0, atol=1e-12)
