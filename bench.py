@@ -147,7 +147,7 @@ def measured_traffic(workload: str):
     return float(rec["hbm_bytes_per_launch"]), os.path.relpath(path, ROOT)
 
 
-def packed_clip(w: synth.Workload, reps: int = 3) -> dict:
+def packed_clip(w: synth.Workload, reps: int = 3, backward: bool = True) -> dict:
     """ff_packed_attention over the workload's whole clip at one stage and layer.
 
     Q, K, V of all chunks in one token-major array, the anchor frames of
@@ -185,11 +185,43 @@ def packed_clip(w: synth.Workload, reps: int = 3) -> dict:
     avg = float(np.mean(ms))
     tf = flops / (avg * 1e-3) / 1e12
     log(f"packed clip attention: {n} chunks in one launch, {avg:.2f} ms = {tf:.1f} TFLOP/s")
+    result = {"chunks": n, "window": w.ring_chunks, "anchor_frames_total": len(frames),
+              "ms_per_launch": round(avg, 3), "tflops": round(tf, 2),
+              "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2)}
+    if backward:
+        # backward of the same launch: forward with its log-sum-exp, then the four
+        # backward launches; FLOPs counted as 2.5x the forward (the usual five
+        # products), the kernels run eight (S three times, dP twice)
+        lse = torch.empty((n * Nq, w.heads), dtype=torch.float32, device=dev)
+        dout = torch.randn(shape, generator=g, device=dev).to(w.torch_dtype)
+        ff.packed_attention(q, k, v, n_chunks=n, window=w.ring_chunks, anchor_k=ak, anchor_v=av,
+                            frame_tokens=G, anchors_of_chunk=table, out=out, lse=lse)
+
+        def bwd():
+            return ff.packed_attention_bwd(q, k, v, out, dout, lse, n_chunks=n, window=w.ring_chunks,
+                                           anchor_k=ak, anchor_v=av, frame_tokens=G,
+                                           anchors_of_chunk=table)
+        grads = bwd()
+        torch.cuda.synchronize()
+        del grads
+        evb = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        evb[0].record(stream)
+        for r in range(reps):
+            grads = bwd()
+            evb[r + 1].record(stream)
+            del grads
+        torch.cuda.synchronize()
+        bms = float(np.mean([evb[r].elapsed_time(evb[r + 1]) for r in range(reps)]))
+        btf = 2.5 * flops / (bms * 1e-3) / 1e12
+        log(f"packed clip backward: {bms:.2f} ms = {btf:.1f} TFLOP/s (2.5x forward FLOPs), "
+            f"{4.0 * flops / (bms * 1e-3) / 1e12:.1f} TFLOP/s of matrix work issued")
+        result["backward"] = {"ms_per_call": round(bms, 3), "tflops_2p5x_forward": round(btf, 2),
+                              "tflops_issued": round(4.0 * flops / (bms * 1e-3) / 1e12, 2),
+                              "pct_bf16_peak_issued": round(100 * 4.0 * flops / (bms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2)}
+        del lse, dout
     del q, k, v, out, ak, av
     torch.cuda.empty_cache()
-    return {"chunks": n, "window": w.ring_chunks, "anchor_frames_total": len(frames),
-            "ms_per_launch": round(avg, 3), "tflops": round(tf, 2),
-            "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2)}
+    return result
 
 
 def wavefront_clip(name: str = "1.3b-480p") -> dict:

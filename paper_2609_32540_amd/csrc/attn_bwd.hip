@@ -149,6 +149,12 @@ __device__ inline void rows_times_b(const char* tile, int kb, int a_lane, const 
     const bf16x8 a = *reinterpret_cast<const bf16x8*>(base + (a_lane ^ (ks << 5)));
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, breg[ks], acc, 0, 0, 0);
   }
+  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    if (ks + 2 < D / 16) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
 }
 
 // out[db] += (rows kb*32 .. +31 of the tile)^T x P, P packed bf16 from the
@@ -200,6 +206,46 @@ __device__ inline void load_b(const __bf16* base, int64_t row_elems, int col0, i
   const __bf16* p = base + int64_t(r) * row_elems + 8 * (lane >> 5);
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks) breg[ks] = *reinterpret_cast<const bf16x8*>(p + 16 * ks);
+}
+
+// Stationary operand kept in LDS instead of registers (register budget): the
+// 32 rows of wave w at stat + (32 w + r) * ROWB, 16-byte chunks swizzled as in
+// the tiles, so reading it back as a B operand is conflict-free.
+template <int D>
+__device__ inline void stash_b(char* stat, const __bf16* base, int64_t row_elems, int col0, int n,
+                               int wave, int lane) {
+  // lane l writes chunks l % CPR (and l % CPR + ..) of rows: 64 lanes cover 64 * 16 B per pass
+  constexpr int CPR = Cfg<D>::CPR;
+#pragma unroll
+  for (int pass = 0; pass < 32 * CPR / 64; ++pass) {
+    const int idx = pass * 64 + lane;
+    const int r = idx / CPR, ch = idx % CPR;
+    const int src = min(col0 + r, n - 1);
+    const u32x4 v = *reinterpret_cast<const u32x4*>(base + int64_t(src) * row_elems + 8 * ch);
+    *reinterpret_cast<u32x4*>(stat + (32 * wave + r) * Cfg<D>::ROWB + ((ch ^ swz<D>(r)) << 4)) = v;
+  }
+}
+
+// acc = A(rows kb*32 .. +31 of the tile) x B^T with B read from the stash
+template <int D>
+__device__ inline void rows_times_stash(const char* tile, int kb, int a_lane, const char* stat_w,
+                                        f32x16& acc) {
+#pragma unroll
+  for (int j = 0; j < 16; ++j) acc[j] = 0.0f;
+  const char* base = tile + kb * 32 * Cfg<D>::ROWB;
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    const bf16x8 a = *reinterpret_cast<const bf16x8*>(base + (a_lane ^ (ks << 5)));
+    const bf16x8 b = *reinterpret_cast<const bf16x8*>(stat_w + (a_lane ^ (ks << 5)));
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+  }
+  // operands read two products ahead at most (register budget)
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    if (ks + 2 < D / 16) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
 }
 
 // store scale * acc^T: acc rows = d (32 db + 8 (j/4) + 4 half + j%4), columns = lanes
@@ -256,6 +302,7 @@ void bwd_dq_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout
   using C = Cfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
   __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
+  __shared__ __attribute__((aligned(1024))) char stash[kBlockN * C::ROWB];
   const int nq = plan.chunk_tokens;
   const int logical = xcd_logical(blockIdx.x, gridDim.x);
   const int chunk = logical / (heads * n_qtiles);
@@ -266,9 +313,10 @@ void bwd_dq_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout
   const int64_t row_elems = int64_t(heads) * D;
   const int q0 = qt * kBlockN + wave * 32;
 
-  bf16x8 qreg[C::KS], dreg[C::KS];
+  bf16x8 qreg[C::KS];
   load_b<D>(q + tok0 * row_elems + head * D, row_elems, q0, nq, lane, qreg);
-  load_b<D>(dout + tok0 * row_elems + head * D, row_elems, q0, nq, lane, dreg);
+  stash_b<D>(stash, dout + tok0 * row_elems + head * D, row_elems, q0, nq, wave, lane);
+  const char* stash_w = stash + 32 * wave * C::ROWB;
   const int qi = min(q0 + l32, nq - 1);
   const float L = lse[(tok0 + qi) * heads + head];
   const float Dq = delta[(tok0 + qi) * heads + head];
@@ -314,7 +362,7 @@ void bwd_dq_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout
       f32x16 s, dp;
       rows_times_b<D>(cur, kb, ln.a_lane, qreg, s);              // S^T = K Q^T
       __builtin_amdgcn_sched_barrier(0);
-      rows_times_b<D>(cur + C::TILE, kb, ln.a_lane, dreg, dp);   // dP^T = V dO^T
+      rows_times_stash<D>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);   // dP^T = V dO^T
       __builtin_amdgcn_sched_barrier(0);
       uint32_t pk[8];
 #pragma unroll
@@ -362,6 +410,7 @@ void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dou
   using C = Cfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
   __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
+  __shared__ __attribute__((aligned(1024))) char stash[kDK ? kBlockN * C::ROWB : 16];
   const int nq = plan.chunk_tokens, G = plan.frame_tokens;
   const int n_units = plan.n_chunks * ku.kpc + ku.n_frames * ku.kpf;
   const int logical = xcd_logical(blockIdx.x, gridDim.x);
@@ -390,9 +439,10 @@ void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dou
     obase = dk_anchor + int64_t(owner) * G * row_elems;
   }
   const int k0 = k_first + wave * 32;
-  bf16x8 kreg[C::KS], vreg[C::KS];
+  bf16x8 kreg[C::KS];
   load_b<D>(kbase + head * D, row_elems, k0, n_keys, lane, kreg);
-  if constexpr (kDK) load_b<D>(vbase + head * D, row_elems, k0, n_keys, lane, vreg);
+  if constexpr (kDK) stash_b<D>(stash, vbase + head * D, row_elems, k0, n_keys, wave, lane);
+  const char* stash_w = stash + (kDK ? 32 * wave * C::ROWB : 0);
   f32x16 acc[C::DB];
 #pragma unroll
   for (int db = 0; db < C::DB; ++db)
@@ -453,7 +503,7 @@ void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dou
       rows_times_b<D>(cur, kb, ln.a_lane, kreg, s);               // S = Q K^T (rows = queries)
       __builtin_amdgcn_sched_barrier(0);
       f32x16 dp;
-      if constexpr (kDK) rows_times_b<D>(cur + C::TILE, kb, ln.a_lane, vreg, dp);   // dP = dO V^T
+      if constexpr (kDK) rows_times_stash<D>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);   // dP = dO V^T
       __builtin_amdgcn_sched_barrier(0);
       uint32_t pk[8];
 #pragma unroll
