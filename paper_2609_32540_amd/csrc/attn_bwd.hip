@@ -401,12 +401,17 @@ struct KeyUnits {
   uint8_t frame_runs[FF_MAX_ANCHOR_FRAMES * 8][16];   // per anchor frame: (first chunk, count) pairs
 };
 
-template <int D, bool kDK>
+// kMode: 0 = dV only, 1 = dK only, 2 = both in one pass (d = 64, where the
+// registers allow it)
+template <int D, int kMode>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout,
                     const float* __restrict__ lse, const float* __restrict__ delta,
-                    __bf16* __restrict__ dk_chunks, __bf16* __restrict__ dk_anchor, int heads,
+                    __bf16* __restrict__ dk_chunks, __bf16* __restrict__ dk_anchor,
+                    __bf16* __restrict__ dv_chunks, __bf16* __restrict__ dv_anchor, int heads,
                     float c_log2, float scale, PackedPlan plan, KeyUnits ku) {
+  constexpr bool kDK = kMode != 0;   // dK (needs dP)
+  constexpr bool kDV = kMode != 1;
   using C = Cfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
   __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
@@ -421,14 +426,15 @@ void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dou
   const bool is_chunk = unit < plan.n_chunks * ku.kpc;
   int owner, k_first, n_keys;
   const __bf16 *kbase, *vbase;
-  __bf16* obase;
+  __bf16 *obase_k, *obase_v;
   if (is_chunk) {
     owner = unit / ku.kpc;
     k_first = (unit % ku.kpc) * kBlockN;
     n_keys = nq;
     kbase = static_cast<const __bf16*>(plan.k) + int64_t(owner) * nq * row_elems;
     vbase = static_cast<const __bf16*>(plan.v) + int64_t(owner) * nq * row_elems;
-    obase = dk_chunks + int64_t(owner) * nq * row_elems;
+    obase_k = dk_chunks + int64_t(owner) * nq * row_elems;
+    obase_v = dv_chunks + int64_t(owner) * nq * row_elems;
   } else {
     const int a = unit - plan.n_chunks * ku.kpc;
     owner = a / ku.kpf;
@@ -436,18 +442,25 @@ void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dou
     n_keys = G;
     kbase = static_cast<const __bf16*>(plan.ak) + int64_t(owner) * G * row_elems;
     vbase = static_cast<const __bf16*>(plan.av) + int64_t(owner) * G * row_elems;
-    obase = dk_anchor + int64_t(owner) * G * row_elems;
+    obase_k = dk_anchor + int64_t(owner) * G * row_elems;
+    obase_v = dv_anchor + int64_t(owner) * G * row_elems;
   }
   const int k0 = k_first + wave * 32;
   bf16x8 kreg[C::KS];
   load_b<D>(kbase + head * D, row_elems, k0, n_keys, lane, kreg);
   if constexpr (kDK) stash_b<D>(stash, vbase + head * D, row_elems, k0, n_keys, wave, lane);
   const char* stash_w = stash + (kDK ? 32 * wave * C::ROWB : 0);
-  f32x16 acc[C::DB];
+  f32x16 acc[C::DB], acc_v[kMode == 2 ? C::DB : 1];
 #pragma unroll
   for (int db = 0; db < C::DB; ++db)
 #pragma unroll
     for (int j = 0; j < 16; ++j) acc[db][j] = 0.0f;
+  if constexpr (kMode == 2) {
+#pragma unroll
+    for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) acc_v[db][j] = 0.0f;
+  }
 
   // query runs of this unit
   Stream<D, true> st;
@@ -505,25 +518,36 @@ void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dou
       f32x16 dp;
       if constexpr (kDK) rows_times_stash<D>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);   // dP = dO V^T
       __builtin_amdgcn_sched_barrier(0);
-      uint32_t pk[8];
+      uint32_t pk[8], pv[8];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int r0 = kb * 32 + 8 * g + 4 * half;
         const f32x4 Lr = *reinterpret_cast<const f32x4*>(lse_t + r0);
         f32x4 Dr;
         if constexpr (kDK) Dr = *reinterpret_cast<const f32x4*>(del_t + r0);
-        float v4[4];
+        float v4[4], p4[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float p = r0 + e < nv ? __builtin_amdgcn_exp2f(fmaf(s[4 * g + e], c_log2, -Lr[e])) : 0.0f;
+          p4[e] = p;
           if constexpr (kDK) v4[e] = p * (dp[4 * g + e] - Dr[e]);
-          else v4[e] = p;
         }
-        pk[2 * g] = pack_bf16(v4[0], v4[1]);
-        pk[2 * g + 1] = pack_bf16(v4[2], v4[3]);
+        if constexpr (kDK) {
+          pk[2 * g] = pack_bf16(v4[0], v4[1]);
+          pk[2 * g + 1] = pack_bf16(v4[2], v4[3]);
+        }
+        if constexpr (kDV) {
+          pv[2 * g] = pack_bf16(p4[0], p4[1]);
+          pv[2 * g + 1] = pack_bf16(p4[2], p4[3]);
+        }
       }
       // dV^T += dO^T P, dK^T += Q^T dS
-      rows_t_times_p<D>(kDK ? cur : cur + C::TILE, kb, ln.t_lane, pk, acc);
+      if constexpr (kMode == 0) rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc);
+      if constexpr (kMode == 1) rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);
+      if constexpr (kMode == 2) {
+        rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc_v);
+        rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);
+      }
       __builtin_amdgcn_sched_barrier(0);   // one 32-query block at a time (register budget)
     }
     st.advance(csg, ck0);
@@ -535,7 +559,12 @@ void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dou
     tile(t, lds1, lds0);
     ++t;
   }
-  store_t<D>(obase + head * D, row_elems, k0 + l32, n_keys, lane, acc, kDK ? scale : 1.0f);
+  if constexpr (kMode == 0) store_t<D>(obase_v + head * D, row_elems, k0 + l32, n_keys, lane, acc, 1.0f);
+  if constexpr (kMode == 1) store_t<D>(obase_k + head * D, row_elems, k0 + l32, n_keys, lane, acc, scale);
+  if constexpr (kMode == 2) {
+    store_t<D>(obase_k + head * D, row_elems, k0 + l32, n_keys, lane, acc, scale);
+    store_t<D>(obase_v + head * D, row_elems, k0 + l32, n_keys, lane, acc_v, 1.0f);
+  }
 }
 
 }  // namespace
@@ -564,24 +593,22 @@ hipError_t launch_attention_bwd_bf16(const void* q, const void* out, const void*
   const dim3 g_q(unsigned(plan.n_chunks * heads * n_qtiles)), g_k(unsigned(n_units * heads));
   const __bf16* qp = static_cast<const __bf16*>(q);
   const __bf16* dp = static_cast<const __bf16*>(dout);
+  __bf16 *dkp = static_cast<__bf16*>(dk), *dvp = static_cast<__bf16*>(dv);
+  __bf16 *dakp = static_cast<__bf16*>(dak), *davp = static_cast<__bf16*>(dav);
+  // dV and dK in separate passes: one fused pass needs both accumulators at once,
+  // more registers than two waves per SIMD leave
   if (head_dim == 128) {
     hipLaunchKernelGGL(bwd_dq_kernel<128>, g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
                        static_cast<__bf16*>(dq), heads, c_log2, softmax_scale, plan, n_qtiles);
-    hipLaunchKernelGGL((bwd_dkv_kernel<128, false>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
-                       delta, static_cast<__bf16*>(dv), static_cast<__bf16*>(dav), heads, c_log2,
-                       softmax_scale, plan, ku);
-    hipLaunchKernelGGL((bwd_dkv_kernel<128, true>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
-                       delta, static_cast<__bf16*>(dk), static_cast<__bf16*>(dak), heads, c_log2,
-                       softmax_scale, plan, ku);
+    hipLaunchKernelGGL((bwd_dkv_kernel<128, 0>), g_k, dim3(kThreads), 0, stream, qp, dp, lse, delta,
+                       dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
+    hipLaunchKernelGGL((bwd_dkv_kernel<128, 1>), g_k, dim3(kThreads), 0, stream, qp, dp, lse, delta,
+                       dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
   } else {
     hipLaunchKernelGGL(bwd_dq_kernel<64>, g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
                        static_cast<__bf16*>(dq), heads, c_log2, softmax_scale, plan, n_qtiles);
-    hipLaunchKernelGGL((bwd_dkv_kernel<64, false>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
-                       delta, static_cast<__bf16*>(dv), static_cast<__bf16*>(dav), heads, c_log2,
-                       softmax_scale, plan, ku);
-    hipLaunchKernelGGL((bwd_dkv_kernel<64, true>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
-                       delta, static_cast<__bf16*>(dk), static_cast<__bf16*>(dak), heads, c_log2,
-                       softmax_scale, plan, ku);
+    hipLaunchKernelGGL((bwd_dkv_kernel<64, 2>), g_k, dim3(kThreads), 0, stream, qp, dp, lse, delta,
+                       dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
   }
   return hipGetLastError();
 }
