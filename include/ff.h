@@ -174,7 +174,12 @@ ff_status ff_anchor_set(ff_cache* cache, int32_t layer, int32_t n_frames, const 
  * or it is empty); FF_ERR_ORDER otherwise.  bf16: products on bf16 matrix
  * cores with float32 accumulation, softmax in float32, probabilities and
  * output rounded to bf16 (nearest even).  f32: float32 throughout.
- * softmax_scale is normally 1/sqrt(head_dim). */
+ * softmax_scale is normally 1/sqrt(head_dim).
+ * bf16 launches whose last round of workgroups is partial run that round's
+ * work as key parts whose partial results go to a per-stage scratch region
+ * of the cache buffer, merged by a second kernel on the same stream: calls of
+ * one stage (any layer) that overlap in time on different streams race on
+ * it, so order them on one stream (different stages are independent). */
 ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
                              const void* q, const void* k_cur, const void* v_cur, void* out,
                              float softmax_scale, void* stream);

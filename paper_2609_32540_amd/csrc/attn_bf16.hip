@@ -56,6 +56,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -138,7 +139,7 @@ struct Cursor {
 template <int D, class Src>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, int nq, int heads,
-                      float scale_log2, Src src, int n_qtiles) {
+                      float scale_log2, Src src, int n_qtiles, TailSplit tail) {
   constexpr bool kPacked = __is_same(Src, PackedPlan);
   using C = Cfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
@@ -148,11 +149,21 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
 
   // XCD-aware renumbering: hardware block b runs on XCD b % 8; give each XCD a
   // contiguous range of logical tiles.
-  const int n_wg = gridDim.x;
+  // (the tail-round workgroups b >= tail.n_full take part tail.split of one
+  // unit's key tiles each)
   const int b = blockIdx.x;
-  const int xcd = b % kXcds, idx = b / kXcds;
-  const int per = n_wg / kXcds, rem = n_wg % kXcds;
-  const int logical = xcd * per + min(xcd, rem) + idx;
+  int logical, part_id = 0, n_parts = 1;
+  if (b < tail.n_full) {
+    const int n_wg = tail.n_full;
+    const int xcd = b % kXcds, idx = b / kXcds;
+    const int per = n_wg / kXcds, rem = n_wg % kXcds;
+    logical = xcd * per + min(xcd, rem) + idx;
+  } else {
+    const int j = b - tail.n_full;
+    logical = tail.n_full + j / tail.split;
+    part_id = j % tail.split;
+    n_parts = tail.split;
+  }
   int chunk = 0, rest = logical;
   if constexpr (kPacked) {
     chunk = logical / (heads * n_qtiles);
@@ -221,6 +232,9 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   // number of tiles
   int n_tiles = 0;
   for (int i = 0; i < n_segs; ++i) n_tiles += (seg_len(i) + kBK - 1) / kBK;
+  // this workgroup's share of the tiles: [t_begin, t_begin + n_tiles)
+  const int t_begin = part_id * n_tiles / n_parts;
+  n_tiles = (part_id + 1) * n_tiles / n_parts - t_begin;
   auto advance = [&](Cursor c) {
     c.k0 += kBK;
     if (c.k0 >= seg_len(c.sg)) {
@@ -381,6 +395,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
 
   // ---- prologue: tiles 0 and 1 in flight, S^T of tile 0 -----------------------------
   Cursor c_next = {0, 0};                    // the tile whose S^T the iteration computes
+  for (int i = 0; i < t_begin; ++i) c_next = advance(c_next);
   Cursor c_dma = advance(c_next);            // the tile the iteration copies
   issue_tile(lds0, c_next);
   if (n_tiles > 1) {
@@ -393,7 +408,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   compute_s(lds0, 0, s_cur);
   compute_s(lds0, 1, s_cur);
   {
-    const int nv = min(kBK, seg_len(0));
+    const int nv = min(kBK, seg_len(c_next.sg) - c_next.k0);
     if (nv < kBK) mask_s(s_cur, nv);
   }
   update_max(s_cur);
@@ -490,7 +505,25 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       if (src.lse != nullptr && half == 0 && qi < nq)
         src.lse[(int64_t(chunk) * nq + qi) * heads + head] = m_run[cb] + log2f(l_tot);
     }
-    if (qi < nq) {
+    if (n_parts > 1) {
+      // unnormalised partial result of this part: O (row = query of the
+      // workgroup), the reference max and the sum, merged by the tail kernel
+      float* pb = tail.part + size_t((logical - tail.n_full) * n_parts + part_id) *
+                                  (kBlockQ * D + 2 * kBlockQ);
+      const int row = wave * kWaveQ + 32 * cb + l32;
+#pragma unroll
+      for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const f32x4 v = {o[cb][db][4 * a + 0], o[cb][db][4 * a + 1], o[cb][db][4 * a + 2],
+                           o[cb][db][4 * a + 3]};
+          *reinterpret_cast<f32x4*>(pb + row * D + 32 * db + 8 * a + 4 * half) = v;
+        }
+      if (half == 0) {
+        pb[kBlockQ * D + row] = m_run[cb];
+        pb[kBlockQ * D + kBlockQ + row] = l_tot;
+      }
+    } else if (qi < nq) {
       __bf16* op = out + (int64_t(qi) * heads + head) * D + 4 * half;
 #pragma unroll
       for (int db = 0; db < C::DB; ++db)
@@ -505,23 +538,86 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   }
 }
 
+// Merge of the tail parts: thread = (tail unit, query row, 8 values of d).
+template <int D>
+__global__ __launch_bounds__(256) void tail_merge_kernel(const float* __restrict__ part,
+                                                         __bf16* __restrict__ out, int nq, int heads,
+                                                         int n_qtiles, TailSplit tail, int n_units) {
+  constexpr int CH = D / 8;
+  const int64_t tid = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (tid >= int64_t(n_units) * kBlockQ * CH) return;
+  const int u = int(tid / (kBlockQ * CH));
+  const int rem = int(tid % (kBlockQ * CH));
+  const int row = rem / CH, ch = rem % CH;
+  const int unit = tail.n_full + u;
+  const int head = unit / n_qtiles, qt = unit % n_qtiles;
+  const int qi = qt * kBlockQ + row;
+  if (qi >= nq) return;
+  const size_t stride = size_t(kBlockQ) * D + 2 * kBlockQ;
+  const float* p0 = part + size_t(u) * tail.split * stride;
+  float m = -INFINITY;
+  for (int s = 0; s < tail.split; ++s) m = fmaxf(m, p0[s * stride + kBlockQ * D + row]);
+  float l = 0.0f, acc[8] = {};
+  for (int s = 0; s < tail.split; ++s) {
+    const float* ps = p0 + s * stride;
+    const float w = __builtin_amdgcn_exp2f(ps[kBlockQ * D + row] - m);
+    l += w * ps[kBlockQ * D + kBlockQ + row];
+    const f32x4 a = *reinterpret_cast<const f32x4*>(ps + row * D + 8 * ch);
+    const f32x4 b = *reinterpret_cast<const f32x4*>(ps + row * D + 8 * ch + 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[e] += w * a[e];
+      acc[4 + e] += w * b[e];
+    }
+  }
+  const float inv = 1.0f / l;
+  u32x4 w4;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) w4[e] = pack_bf16(acc[2 * e] * inv, acc[2 * e + 1] * inv);
+  *reinterpret_cast<u32x4*>(out + (int64_t(qi) * heads + head) * D + 8 * ch) = w4;
+}
+
 }  // namespace
 
+int attention_bf16_units(int nq, int heads) { return heads * ((nq + kBlockQ - 1) / kBlockQ); }
+
+int attention_bf16_key_tiles(const KvSegments& segs) {
+  int n = 0;
+  for (int i = 0; i < segs.n; ++i) n += (segs.seg[i].len + kBK - 1) / kBK;
+  return n;
+}
+
+size_t attention_bf16_part_bytes(int head_dim) {
+  return size_t(kBlockQ) * head_dim * 4 + 2 * kBlockQ * 4;
+}
+
 hipError_t launch_attention_bf16(const void* q, void* out, int nq, int heads, int head_dim,
-                                 float softmax_scale, const KvSegments& segs,
+                                 float softmax_scale, const KvSegments& segs, const TailSplit& tail,
                                  hipStream_t stream) {
   if (nq <= 0) return hipSuccess;
   const int n_qtiles = (nq + kBlockQ - 1) / kBlockQ;
-  const dim3 grid(n_qtiles * heads);
+  const int units = n_qtiles * heads;
+  const int n_tail = units - tail.n_full;
+  const dim3 grid(tail.n_full + n_tail * tail.split);
   const float scale_log2 = float(double(softmax_scale) * 1.4426950408889634);
   if (head_dim == 128)
     hipLaunchKernelGGL((attn_bf16_kernel<128, KvSegments>), grid, dim3(kThreads), 0, stream,
                        static_cast<const __bf16*>(q), static_cast<__bf16*>(out), nq, heads,
-                       scale_log2, segs, n_qtiles);
+                       scale_log2, segs, n_qtiles, tail);
   else
     hipLaunchKernelGGL((attn_bf16_kernel<64, KvSegments>), grid, dim3(kThreads), 0, stream,
                        static_cast<const __bf16*>(q), static_cast<__bf16*>(out), nq, heads,
-                       scale_log2, segs, n_qtiles);
+                       scale_log2, segs, n_qtiles, tail);
+  if (tail.split > 1 && n_tail > 0) {
+    const int64_t threads = int64_t(n_tail) * kBlockQ * (head_dim / 8);
+    const dim3 g(unsigned((threads + 255) / 256));
+    if (head_dim == 128)
+      hipLaunchKernelGGL(tail_merge_kernel<128>, g, dim3(256), 0, stream, tail.part,
+                         static_cast<__bf16*>(out), nq, heads, n_qtiles, tail, n_tail);
+    else
+      hipLaunchKernelGGL(tail_merge_kernel<64>, g, dim3(256), 0, stream, tail.part,
+                         static_cast<__bf16*>(out), nq, heads, n_qtiles, tail, n_tail);
+  }
   return hipGetLastError();
 }
 
@@ -533,14 +629,15 @@ hipError_t launch_attention_bf16_packed(const void* q, void* out, int heads, int
   const int n_qtiles = (nq + kBlockQ - 1) / kBlockQ;
   const dim3 grid(plan.n_chunks * n_qtiles * heads);
   const float scale_log2 = float(double(softmax_scale) * 1.4426950408889634);
+  const TailSplit whole = {int(grid.x), 1, nullptr};
   if (head_dim == 128)
     hipLaunchKernelGGL((attn_bf16_kernel<128, PackedPlan>), grid, dim3(kThreads), 0, stream,
                        static_cast<const __bf16*>(q), static_cast<__bf16*>(out), nq, heads,
-                       scale_log2, plan, n_qtiles);
+                       scale_log2, plan, n_qtiles, whole);
   else
     hipLaunchKernelGGL((attn_bf16_kernel<64, PackedPlan>), grid, dim3(kThreads), 0, stream,
                        static_cast<const __bf16*>(q), static_cast<__bf16*>(out), nq, heads,
-                       scale_log2, plan, n_qtiles);
+                       scale_log2, plan, n_qtiles, whole);
   return hipGetLastError();
 }
 

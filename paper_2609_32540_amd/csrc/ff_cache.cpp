@@ -56,8 +56,16 @@ struct Layout {
   size_t slot_tensor_bytes;   // one of K / V of one ring slot
   size_t anchor_base;         // offset of layer 0's anchor K
   size_t ring_base;           // offset of (stage 0, layer 0, slot 0) K
+  size_t tail_base;           // offset of stage 0's tail-split partials (bf16 only)
+  size_t tail_stage_bytes;    // partials of one stage
+  int tail_slots;             // partials per stage
   size_t total;
 };
+
+// Tail split: at most this many key parts per unit, and partial slots for up
+// to kTailUnits units (one round of workgroups on a 256-CU device).
+constexpr int kMaxTailSplit = 4;
+constexpr int kTailUnits = 256;
 
 ff_status check_desc(const ff_cache_desc* d) {
   if (!d) return fail(FF_ERR_INVALID_ARG, "desc is NULL");
@@ -99,8 +107,16 @@ Layout make_layout(const ff_cache_desc* d) {
   L.slot_tensor_bytes = align_up(L.chunk_tokens * d->num_heads * row);
   L.anchor_base = 0;
   L.ring_base = L.anchor_base + 2 * L.anchor_tensor_bytes * d->num_layers;
-  L.total = L.ring_base +
-            2 * L.slot_tensor_bytes * size_t(d->ring_chunks) * d->num_layers * d->num_stages;
+  L.tail_base = L.ring_base +
+                2 * L.slot_tensor_bytes * size_t(d->ring_chunks) * d->num_layers * d->num_stages;
+  L.tail_slots = 0;
+  L.tail_stage_bytes = 0;
+  if (d->dtype == FF_DT_BF16) {
+    const int units = ff::attention_bf16_units(int(L.chunk_tokens), d->num_heads);
+    L.tail_slots = kMaxTailSplit * std::min(units, kTailUnits);
+    L.tail_stage_bytes = align_up(size_t(L.tail_slots) * ff::attention_bf16_part_bytes(d->head_dim));
+  }
+  L.total = L.tail_base + L.tail_stage_bytes * d->num_stages;
   return L;
 }
 
@@ -125,6 +141,9 @@ struct ff_cache {
     return dev + layout.ring_base + i * layout.slot_tensor_bytes;
   }
   char* slot_v(int s, int l, int slot) const { return slot_k(s, l, slot) + layout.slot_tensor_bytes; }
+  float* tail_part(int s) const {
+    return reinterpret_cast<float*>(dev + layout.tail_base + size_t(s) * layout.tail_stage_bytes);
+  }
   int row_bytes() const { return int(layout.elem_bytes) * desc.head_dim; }
 };
 
@@ -143,6 +162,41 @@ ff_status check_aligned(const void* p, const char* name) {
   if (reinterpret_cast<uintptr_t>(p) % 16 != 0)
     return fail(FF_ERR_INVALID_ARG, "%s must be 16-byte aligned", name);
   return FF_OK;
+}
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+      n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
+// Split of the last round of `units` equal workgroups of n_tiles key tiles
+// each over `cus` compute units: the units of the partial round run as up
+// to kMaxTailSplit key parts (at least 8 tiles each) when that shortens the
+// round, estimated as ceil(parts / cus) / split of a whole workgroup.
+ff::TailSplit choose_tail_split(int units, int n_tiles, int cus, int slots, float* part) {
+  ff::TailSplit t = {units, 1, part};
+  const int n_tail = units % cus;
+  if (n_tail == 0 || part == nullptr) return t;
+  double best = 1.0;
+  for (int s = 2; s <= kMaxTailSplit; ++s) {
+    if (n_tiles < 8 * s || n_tail * s > slots) break;
+    const double cost = double((n_tail * s + cus - 1) / cus) / s;
+    if (cost < best - 1e-9) {
+      best = cost;
+      t.split = s;
+    }
+  }
+  if (t.split > 1) t.n_full = units - n_tail;
+  return t;
 }
 
 ff_status hip_status(hipError_t e, const char* what) {
@@ -364,9 +418,14 @@ ff_status chunk_attention_impl(ff_cache* cache, int32_t stage, int32_t layer, in
   add(k_cur, v_cur, D, heads * D, chunk_tokens);
 
   hipError_t e;
-  if (d.dtype == FF_DT_BF16)
-    e = ff::launch_attention_bf16(q, out, chunk_tokens, heads, D, softmax_scale, segs,
+  if (d.dtype == FF_DT_BF16) {
+    const ff::TailSplit tail =
+        choose_tail_split(ff::attention_bf16_units(chunk_tokens, heads),
+                          ff::attention_bf16_key_tiles(segs), device_cus(),
+                          cache->layout.tail_slots, cache->tail_part(stage));
+    e = ff::launch_attention_bf16(q, out, chunk_tokens, heads, D, softmax_scale, segs, tail,
                                   static_cast<hipStream_t>(stream));
+  }
   else
     e = ff::launch_attention_f32(q, out, chunk_tokens, heads, D, softmax_scale, segs,
                                  static_cast<hipStream_t>(stream));

@@ -102,9 +102,26 @@ hipError_t launch_rope3d(void* q, void* k, int n_tok, int heads, int head_dim, i
                          int grid_w, int tokens_per_frame, const RopeParams& p,
                          hipStream_t stream);
 
+// Key split of the last, partial round of workgroups of a launch: units
+// (head, 256-query tile) 0 .. n_full-1 run whole; every later unit runs as
+// `split` workgroups over consecutive ranges of its key tiles, which write
+// unnormalised fp32 partials (attention_bf16_part_bytes each) to `part`, and a
+// merge kernel combines them.  split == 1 runs every unit whole (part unused).
+struct TailSplit {
+  int32_t n_full;
+  int32_t split;
+  float* part;
+};
+
+// Units (head, 256-query tile) of one launch and the bytes of one partial.
+int attention_bf16_units(int nq, int heads);
+// Key tiles a workgroup of the bf16 kernel walks over the read set segs.
+int attention_bf16_key_tiles(const KvSegments& segs);
+size_t attention_bf16_part_bytes(int head_dim);
+
 hipError_t launch_attention_bf16(const void* q, void* out, int nq, int heads, int head_dim,
                                  float softmax_scale, const KvSegments& segs,
-                                 hipStream_t stream);
+                                 const TailSplit& tail, hipStream_t stream);
 
 hipError_t launch_attention_f32(const void* q, void* out, int nq, int heads, int head_dim,
                                 float softmax_scale, const KvSegments& segs,

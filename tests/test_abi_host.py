@@ -49,7 +49,13 @@ def test_cache_bytes_layout():
     anchor = 3 * 1560 * 12 * 128 * 2
     slot = 4680 * 12 * 128 * 2
     align = lambda x: (x + 255) // 256 * 256
-    assert L.ff_cache_bytes(ctypes.byref(d)) == 2 * 2 * align(anchor) + 4 * 2 * 4 * 2 * align(slot)
+    # tail-split partials per stage: 4 parts x min(units, 256) units of
+    # (256 x 128 + 2 x 256) floats; units = 12 heads x ceil(4680 / 256) = 228
+    tail = 4 * 228 * (256 * 128 + 2 * 256) * 4
+    assert L.ff_cache_bytes(ctypes.byref(d)) == (2 * 2 * align(anchor) + 4 * 2 * 4 * 2 * align(slot)
+                                                 + 4 * align(tail))
+    assert L.ff_cache_bytes(ctypes.byref(desc(dtype=ff.FF_DT_F32))) == (
+        2 * 2 * align(2 * anchor) + 4 * 2 * 4 * 2 * align(2 * slot))
     # C5-shaped, all 4 stages x 40 layers: ~150 GB fits one MI355X
     d5 = desc(num_layers=40, grid_h=45, grid_w=80, num_heads=40)
     assert 140e9 < L.ff_cache_bytes(ctypes.byref(d5)) < 160e9

@@ -202,6 +202,23 @@ def test_attention_degenerate_shapes():
         run.step(c, 0, 0)
 
 
+@pytest.mark.parametrize("head_dim", [64, 128])
+@pytest.mark.parametrize("grid", [(6, 11), (12, 22)])
+def test_attention_tail_split_into_key_parts(head_dim, grid):
+    # Fewer (head, 256-query) units than compute units: the whole launch is
+    # the partial last round, run as 2, 3 or 4 key parts (at least 8 key
+    # tiles of 64 each) plus the merge.  6x11 grid: 198-token chunks, one
+    # ragged query tile; anchors 4 tiles + 4 per chunk, so chunks 2..7 see 16,
+    # 20, 24, 28, 32, 32 tiles (2, 2, 3, 3, 4, 4 parts) with part boundaries
+    # inside segments.  12x22 grid: 792-token chunks = 4 query tiles (last
+    # holds 24 queries), 13 tiles per frame group, up to 104 tiles.
+    w = small("bf16", head_dim, heads=2, grid_h=grid[0], grid_w=grid[1], ring_chunks=6,
+              stages=1, layers=1, n_chunks=8, anchor_rule="fixed:0,7,20", max_anchor_frames=3)
+    run = PairedRun(w, rope=False)
+    for c in range(w.n_chunks):
+        run.step(c, 0, 0)
+
+
 def test_unfilled_slots_poisoned_with_nan_are_never_read():
     w = small("bf16", 128, ring_chunks=4, anchor_rule="fixed:3", max_anchor_frames=3)
     run = PairedRun(w, poison=True)
