@@ -402,16 +402,17 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     issue_tile(lds1, c_dma);
     c_dma = advance(c_dma);                  // tile 2
   }
-  f32x16 s_cur[2][kCB];
+  // S^T of even tiles lives in s_a, of odd tiles in s_b (no copies between them)
+  f32x16 s_a[2][kCB], s_b[2][kCB];
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  compute_s(lds0, 0, s_cur);
-  compute_s(lds0, 1, s_cur);
+  compute_s(lds0, 0, s_a);
+  compute_s(lds0, 1, s_a);
   {
     const int nv = min(kBK, seg_len(c_next.sg) - c_next.k0);
-    if (nv < kBK) mask_s(s_cur, nv);
+    if (nv < kBK) mask_s(s_a, nv);
   }
-  update_max(s_cur);
+  update_max(s_a);
   c_next = advance(c_next);                  // tile 1
 
   // ---- main loop, in two halves per tile ---------------------------------------
@@ -422,17 +423,18 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   // so each SIMD pairs one wave's exponentials with the other's matrix work.
   // Tile t lives in slot t % 4; the last reads of tile t (waves 4-7, h2(t))
   // precede barrier t+2, where waves 0-3 copy tile t+4 into its slot.
-  f32x16 s_nxt[2][kCB];
   uint32_t pk0[kCB][8], pk1[kCB][8];
-  auto h1 = [&](char* v_slot, char* k_slot) __attribute__((always_inline)) {
-    asm volatile("" : "+v"(k_lane), "+v"(v_lane[0]), "+v"(v_lane[1]));
+  auto h1 = [&](char* v_slot, char* k_slot, f32x16 (&s_cur)[2][kCB], f32x16 (&s_nxt)[2][kCB])
+      __attribute__((always_inline)) {
+    asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
     compute_s(k_slot, 0, s_nxt);
     probs(s_cur, 0, pk0);
     pv(v_slot + C::TILE, 0, pk0);
     probs(s_cur, 1, pk1);
   };
-  auto h2 = [&](int t, char* v_slot, char* k_slot) __attribute__((always_inline)) {
-    asm volatile("" : "+v"(k_lane), "+v"(v_lane[0]), "+v"(v_lane[1]));
+  auto h2 = [&](int t, char* v_slot, char* k_slot, f32x16 (&s_nxt)[2][kCB])
+      __attribute__((always_inline)) {
+    asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
     compute_s(k_slot, 1, s_nxt);
     pv(v_slot + C::TILE, 1, pk1);
     if (t + 1 < n_tiles) {
@@ -441,10 +443,6 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       update_max(s_nxt);
       c_next = advance(c_next);
     }
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int cb = 0; cb < kCB; ++cb) s_cur[kb][cb] = s_nxt[kb][cb];
   };
   // barrier t: every wave's copies of tile t+1 have landed, tile t-2 is free
   auto sync = [&]() __attribute__((always_inline)) {
@@ -452,44 +450,46 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     __syncthreads();
   };
   if (wave < kCopyWaves) {
-    auto step = [&](int t, char* s0, char* s1, char* s2) __attribute__((always_inline)) {
+    auto step = [&](int t, char* s0, char* s1, char* s2, f32x16 (&sc)[2][kCB],
+                    f32x16 (&sn)[2][kCB]) __attribute__((always_inline)) {
       sync();
       if (t + 2 < n_tiles) {
         issue_tile(s2, c_dma);
         c_dma = advance(c_dma);
       }
-      h1(s0, s1);
-      h2(t, s0, s1);
+      h1(s0, s1, sc, sn);
+      h2(t, s0, s1, sn);
     };
     for (int t = 0; t < n_tiles;) {
-      step(t, lds0, lds1, lds2);
+      step(t, lds0, lds1, lds2, s_a, s_b);
       if (++t >= n_tiles) break;
-      step(t, lds1, lds2, lds3);
+      step(t, lds1, lds2, lds3, s_b, s_a);
       if (++t >= n_tiles) break;
-      step(t, lds2, lds3, lds0);
+      step(t, lds2, lds3, lds0, s_a, s_b);
       if (++t >= n_tiles) break;
-      step(t, lds3, lds0, lds1);
+      step(t, lds3, lds0, lds1, s_b, s_a);
       ++t;
     }
     sync();   // matches the extra barrier of the last step of waves 4-7
   } else {
     sync();
-    h1(lds0, lds1);
+    h1(lds0, lds1, s_a, s_b);
     // step t: barrier t, h2(t-1), and h1(t) while t < n_tiles; the step with
-    // t = n_tiles only finishes the last tile
-    auto step = [&](int t, char* sp, char* s0, char* s1) __attribute__((always_inline)) {
+    // t = n_tiles only finishes the last tile.  S^T of tile t is in sc.
+    auto step = [&](int t, char* sp, char* s0, char* s1, f32x16 (&sc)[2][kCB],
+                    f32x16 (&sn)[2][kCB]) __attribute__((always_inline)) {
       sync();
-      h2(t - 1, sp, s0);
-      if (t < n_tiles) h1(s0, s1);
+      h2(t - 1, sp, s0, sc);
+      if (t < n_tiles) h1(s0, s1, sc, sn);
     };
     for (int t = 1;;) {
-      step(t, lds0, lds1, lds2);
+      step(t, lds0, lds1, lds2, s_b, s_a);
       if (t++ >= n_tiles) break;
-      step(t, lds1, lds2, lds3);
+      step(t, lds1, lds2, lds3, s_a, s_b);
       if (t++ >= n_tiles) break;
-      step(t, lds2, lds3, lds0);
+      step(t, lds2, lds3, lds0, s_b, s_a);
       if (t++ >= n_tiles) break;
-      step(t, lds3, lds0, lds1);
+      step(t, lds3, lds0, lds1, s_a, s_b);
       if (t++ >= n_tiles) break;
     }
   }
