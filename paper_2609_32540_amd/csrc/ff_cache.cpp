@@ -12,6 +12,7 @@
 
 #include <algorithm>
 #include <array>
+#include <atomic>
 #include <climits>
 #include <cmath>
 #include <cstdarg>
@@ -164,18 +165,19 @@ ff_status check_aligned(const void* p, const char* name) {
   return FF_OK;
 }
 
-// Compute units of the current device (cached per device).
+// Compute units of the current device (queried once per device; a failed
+// query falls back to 256, which only affects the tail-split choice).
 int device_cus() {
-  static int cus[64] = {};
+  static std::atomic<int> cus[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] == 0) {
-    int n = 0;
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
       n = 256;
-    cus[dev] = n;
+    cus[dev].store(n, std::memory_order_relaxed);
   }
-  return cus[dev];
+  return n;
 }
 
 // Split of the last round of `units` equal workgroups of n_tiles key tiles
