@@ -59,11 +59,24 @@ struct Cfg {
   static constexpr int CPR = D / 8;
   static constexpr int RPB = 1024 / ROWB;
   static constexpr int BLOCKS = kBT / RPB;              // 1 KB copies per tile and tensor
-  static constexpr int BLOCKS_PER_WAVE = BLOCKS / kWaves;
   static constexpr int TILE = kBT * ROWB;
   static constexpr int VEC = kBT * 4;                   // one float per streamed row
-  static constexpr int SLOT = 2 * TILE + 2 * VEC;       // tensor A, tensor B, vector A, vector B
   static_assert(BLOCKS % kWaves == 0, "every wave copies the same number of 1 KB blocks");
+};
+
+// Ring schedules.  NS = 2: all eight waves copy tile t+1 after barrier t and
+// then work on tile t in lock step.  NS >= 3: waves 0-3 copy tile t + NS - 2
+// after barrier t and run both 32-row blocks of tile t; their SIMD partners,
+// waves 4-7, run block 1 of tile t-1 and then block 0 of tile t, half a tile
+// later, so one wave's exponentials meet the other's matrix work.  Tile u
+// sits in slot u % NS; its last reads (block 1 by waves 4-7) precede barrier
+// u+2, and its slot is refilled at barrier u + 2 at the earliest.
+template <int NS>
+struct Ring {
+  static_assert(NS >= 2 && NS <= 4, "two to four slots");
+  static constexpr bool kOffset = NS >= 3;
+  static constexpr int kCopyWaves = kOffset ? kWaves / 2 : kWaves;
+  static constexpr int kAhead = kOffset ? NS - 2 : 1;   // tiles copied ahead of the first reader
 };
 
 // the forward's LDS swizzle (conflict-free 16-byte row reads and transposing reads)
@@ -89,16 +102,26 @@ __device__ inline uint64_t readlane_u64(uint64_t v, int lane) {
 // token-major tensors (row r at a + r * row_bytes and b + r * row_bytes, this
 // head's columns) and, with kVec, two float vectors (element r at
 // va + r * vec_bytes and vb + r * vec_bytes).
-template <int D, bool kVec>
+template <int D, bool kVec, int kCopyWaves>
 struct Stream {
   using C = Cfg<D>;
+  static constexpr int BPW = C::BLOCKS / kCopyWaves;   // 1 KB blocks per copying wave and tensor
   int len = 0;
   uint64_t a = 0, b = 0, va = 0, vb = 0;
   uint32_t row_bytes, vec_bytes;
   int n_runs, n_tiles;
   int sg = 0, k0 = 0;    // tile being copied next
-  int cp_row[C::BLOCKS_PER_WAVE], cp_choff[C::BLOCKS_PER_WAVE];
+  int cp_row[BPW], cp_choff[BPW];
   int wave, lane;
+
+  __device__ void init_copy_lanes() {
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      const int r = (wave * BPW + i) * C::RPB + lane / C::CPR;
+      cp_row[i] = r;
+      cp_choff[i] = 16 * ((lane % C::CPR) ^ swz<D>(r));
+    }
+  }
 
   __device__ int run_len(int i) const { return __builtin_amdgcn_readlane(len, i); }
   __device__ void advance(int& s, int& k) const {
@@ -108,18 +131,19 @@ struct Stream {
       k = 0;
     }
   }
-  // copy the next tile into `slot` (rows past a partial tile's end repeat its last row)
+  // copy the next tile into `slot` (rows past a partial tile's end repeat its
+  // last row); called by waves 0 .. kCopyWaves-1
   __device__ void issue(char* slot) {
     const int n = run_len(sg);
     const char* ga = reinterpret_cast<const char*>(readlane_u64(a, sg));
     const char* gb = reinterpret_cast<const char*>(readlane_u64(b, sg));
     const bool partial = k0 + kBT > n;
 #pragma unroll
-    for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
+    for (int i = 0; i < BPW; ++i) {
       int tok = k0 + cp_row[i];
       if (partial) tok = min(tok, n - 1);
       const uint32_t off = uint32_t(tok) * row_bytes + uint32_t(cp_choff[i]);
-      char* dst = slot + (wave * C::BLOCKS_PER_WAVE + i) * 1024;
+      char* dst = slot + (wave * BPW + i) * 1024;
       __builtin_amdgcn_global_load_lds(GLOBAL_PTR(ga + off), LDS_PTR(void, dst), 16, 0, 0);
       __builtin_amdgcn_global_load_lds(GLOBAL_PTR(gb + off), LDS_PTR(void, dst + C::TILE), 16, 0, 0);
     }
@@ -135,6 +159,102 @@ struct Stream {
     advance(sg, k0);
   }
 };
+
+// Drives the tile loop of one workgroup over n > 0 tiles with the Ring<NS>
+// schedule.  issue(slot) copies the stream's next tile into slot (copy waves
+// only); next_nv() returns the valid rows of the next tile this wave works on
+// and advances its cursor; block(slot, kb, nv) works on 32-row block kb of
+// the tile in slot.  Slots are distinct __shared__ arrays, referenced
+// statically (the loops are unrolled by NS), so the compiler never orders a
+// read of one slot behind a copy into another.
+template <int NS, class Issue, class NextNv, class Block>
+__device__ __attribute__((always_inline)) inline void run_ring(int n, int wave, char* s0, char* s1,
+                                                               char* s2, char* s3, Issue& issue,
+                                                               NextNv& next_nv, Block& block) {
+  using R = Ring<NS>;
+  auto sync = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  };
+  if constexpr (!R::kOffset) {
+    issue(s0);
+    auto step = [&](int t, char* cur, char* nxt) __attribute__((always_inline)) {
+      sync();
+      if (t + 1 < n) issue(nxt);
+      const int nv = next_nv();
+      block(cur, 0, nv);
+      block(cur, 1, nv);
+    };
+    for (int t = 0; t < n;) {
+      step(t, s0, s1);
+      if (++t >= n) break;
+      step(t, s1, s0);
+      ++t;
+    }
+  } else if (wave < R::kCopyWaves) {
+    issue(s0);
+    if (R::kAhead > 1 && n > 1) issue(s1);
+    auto step = [&](int t, char* cur, char* ahead) __attribute__((always_inline)) {
+      sync();
+      if (t + R::kAhead < n) issue(ahead);
+      const int nv = next_nv();
+      block(cur, 0, nv);
+      block(cur, 1, nv);
+    };
+    for (int t = 0; t < n;) {
+      if constexpr (NS == 3) {
+        step(t, s0, s1);
+        if (++t >= n) break;
+        step(t, s1, s2);
+        if (++t >= n) break;
+        step(t, s2, s0);
+        ++t;
+      } else {
+        step(t, s0, s2);
+        if (++t >= n) break;
+        step(t, s1, s3);
+        if (++t >= n) break;
+        step(t, s2, s0);
+        if (++t >= n) break;
+        step(t, s3, s1);
+        ++t;
+      }
+    }
+    sync();   // matches the extra barrier of waves 4-7
+  } else {
+    sync();
+    int nv_prev = next_nv();
+    block(s0, 0, nv_prev);
+    // step t: barrier t, block 1 of tile t-1, block 0 of tile t while t < n
+    auto step = [&](int t, char* prev, char* cur) __attribute__((always_inline)) {
+      sync();
+      block(prev, 1, nv_prev);
+      if (t < n) {
+        nv_prev = next_nv();
+        block(cur, 0, nv_prev);
+      }
+    };
+    for (int t = 1;;) {
+      if constexpr (NS == 3) {
+        step(t, s0, s1);
+        if (t++ >= n) break;
+        step(t, s1, s2);
+        if (t++ >= n) break;
+        step(t, s2, s0);
+        if (t++ >= n) break;
+      } else {
+        step(t, s0, s1);
+        if (t++ >= n) break;
+        step(t, s1, s2);
+        if (t++ >= n) break;
+        step(t, s2, s3);
+        if (t++ >= n) break;
+        step(t, s3, s0);
+        if (t++ >= n) break;
+      }
+    }
+  }
+}
 
 // acc[kb] = A(rows kb*32 .. +31 of the tile) x B^T, B the stationary operand
 // (lane (l32, half) holds column l32, elements 16 ks + 8 half .. +7)
@@ -293,16 +413,14 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict
 }
 
 // ---- dQ: query-stationary ---------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void bwd_dq_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout,
-                   const float* __restrict__ lse, const float* __restrict__ delta,
-                   __bf16* __restrict__ dq, int heads, float c_log2, float scale, PackedPlan plan,
-                   int n_qtiles) {
+// Slot = K tile then V tile (the queries' log-sum-exp and D sit in lanes).
+template <int D, int NS>
+__device__ __attribute__((always_inline)) inline void dq_body(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ dout, const float* __restrict__ lse,
+    const float* __restrict__ delta, __bf16* __restrict__ dq, int heads, float c_log2, float scale,
+    const PackedPlan& plan, int n_qtiles, char* s0, char* s1, char* s2, char* s3, char* stash) {
   using C = Cfg<D>;
-  __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
-  __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
-  __shared__ __attribute__((aligned(1024))) char stash[kBlockN * C::ROWB];
+  using R = Ring<NS>;
   const int nq = plan.chunk_tokens;
   const int logical = xcd_logical(blockIdx.x, gridDim.x);
   const int chunk = logical / (heads * n_qtiles);
@@ -326,7 +444,7 @@ void bwd_dq_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout
 #pragma unroll
     for (int j = 0; j < 16; ++j) acc[db][j] = 0.0f;
 
-  Stream<D, false> st;
+  Stream<D, false, R::kCopyWaves> st;
   st.wave = wave;
   st.lane = lane;
   st.row_bytes = uint32_t(2 * row_elems);
@@ -334,61 +452,70 @@ void bwd_dq_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout
 #pragma unroll
   for (int i = 0; i < kMaxRuns; ++i)
     if (lane == i && i < st.n_runs) {
-      const KvSegment s = packed_segment(plan, chunk, i, heads, D, 2);
-      st.len = s.len;
-      st.a = reinterpret_cast<uint64_t>(s.k) + 2ull * uint64_t(head) * D;
-      st.b = reinterpret_cast<uint64_t>(s.v) + 2ull * uint64_t(head) * D;
+      const KvSegment sg = packed_segment(plan, chunk, i, heads, D, 2);
+      st.len = sg.len;
+      st.a = reinterpret_cast<uint64_t>(sg.k) + 2ull * uint64_t(head) * D;
+      st.b = reinterpret_cast<uint64_t>(sg.v) + 2ull * uint64_t(head) * D;
     }
   st.n_tiles = 0;
   for (int i = 0; i < st.n_runs; ++i) st.n_tiles += (st.run_len(i) + kBT - 1) / kBT;
-#pragma unroll
-  for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
-    const int r = (wave * C::BLOCKS_PER_WAVE + i) * C::RPB + lane / C::CPR;
-    st.cp_row[i] = r;
-    st.cp_choff[i] = 16 * ((lane % C::CPR) ^ swz<D>(r));
-  }
+  st.init_copy_lanes();
   Lanes<D> ln(lane);
-  int csg = 0, ck0 = 0;   // tile being computed
+  int csg = 0, ck0 = 0;   // next tile this wave works on
 
-  auto tile = [&](int t, char* cur, char* nxt) __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (t + 1 < st.n_tiles) st.issue(nxt);
+  auto issue = [&](char* slot) __attribute__((always_inline)) { st.issue(slot); };
+  auto next_nv = [&]() __attribute__((always_inline)) {
+    const int nv = min(kBT, st.run_len(csg) - ck0);
+    st.advance(csg, ck0);
+    return nv;
+  };
+  auto block = [&](const char* cur, int kb, int nv) __attribute__((always_inline)) {
     // keep the per-read address arithmetic inside the loop (no hoisted copies)
     asm volatile("" : "+v"(ln.a_lane), "+v"(ln.t_lane[0]), "+v"(ln.t_lane[1]));
-    const int nv = min(kBT, st.run_len(csg) - ck0);
+    f32x16 sv, dp;
+    rows_times_b<D>(cur, kb, ln.a_lane, qreg, sv);                      // S^T = K Q^T
+    __builtin_amdgcn_sched_barrier(0);
+    rows_times_stash<D>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);     // dP^T = V dO^T
+    __builtin_amdgcn_sched_barrier(0);
+    uint32_t pk[8];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x16 s, dp;
-      rows_times_b<D>(cur, kb, ln.a_lane, qreg, s);              // S^T = K Q^T
-      __builtin_amdgcn_sched_barrier(0);
-      rows_times_stash<D>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);   // dP^T = V dO^T
-      __builtin_amdgcn_sched_barrier(0);
-      uint32_t pk[8];
+    for (int j = 0; j < 16; j += 2) {
+      float v2[2];
 #pragma unroll
-      for (int j = 0; j < 16; j += 2) {
-        float v2[2];
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const int key = kb * 32 + 8 * ((j + e) >> 2) + 4 * half + ((j + e) & 3);
-          const float p = key < nv ? __builtin_amdgcn_exp2f(fmaf(s[j + e], c_log2, -L)) : 0.0f;
-          v2[e] = p * (dp[j + e] - Dq);
-        }
-        pk[j >> 1] = pack_bf16(v2[0], v2[1]);
+      for (int e = 0; e < 2; ++e) {
+        const int key = kb * 32 + 8 * ((j + e) >> 2) + 4 * half + ((j + e) & 3);
+        const float p = key < nv ? __builtin_amdgcn_exp2f(fmaf(sv[j + e], c_log2, -L)) : 0.0f;
+        v2[e] = p * (dp[j + e] - Dq);
       }
-      rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);            // dQ^T += K^T dS^T
-      __builtin_amdgcn_sched_barrier(0);   // one 32-key block at a time (register budget)
+      pk[j >> 1] = pack_bf16(v2[0], v2[1]);
     }
-    st.advance(csg, ck0);
+    rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);                     // dQ^T += K^T dS^T
+    __builtin_amdgcn_sched_barrier(0);   // one 32-key block at a time (register budget)
   };
-  if (st.n_tiles > 0) st.issue(lds0);
-  for (int t = 0; t < st.n_tiles;) {
-    tile(t, lds0, lds1);
-    if (++t >= st.n_tiles) break;
-    tile(t, lds1, lds0);
-    ++t;
-  }
+  if (st.n_tiles > 0) run_ring<NS>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv, block);
   store_t<D>(dq + tok0 * row_elems + head * D, row_elems, q0 + l32, nq, lane, acc, scale);
+}
+
+template <int D, int NS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void bwd_dq_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout,
+                   const float* __restrict__ lse, const float* __restrict__ delta,
+                   __bf16* __restrict__ dq, int heads, float c_log2, float scale, PackedPlan plan,
+                   int n_qtiles) {
+  constexpr int kSlot = 2 * Cfg<D>::TILE;
+  __shared__ __attribute__((aligned(1024))) char stash[kBlockN * Cfg<D>::ROWB];
+  __shared__ __attribute__((aligned(1024))) char l0[kSlot];
+  __shared__ __attribute__((aligned(1024))) char l1[kSlot];
+  if constexpr (NS == 2) {
+    dq_body<D, NS>(q, dout, lse, delta, dq, heads, c_log2, scale, plan, n_qtiles, l0, l1, l1, l1, stash);
+  } else if constexpr (NS == 3) {
+    __shared__ __attribute__((aligned(1024))) char l2[kSlot];
+    dq_body<D, NS>(q, dout, lse, delta, dq, heads, c_log2, scale, plan, n_qtiles, l0, l1, l2, l2, stash);
+  } else {
+    __shared__ __attribute__((aligned(1024))) char l2[kSlot];
+    __shared__ __attribute__((aligned(1024))) char l3[kSlot];
+    dq_body<D, NS>(q, dout, lse, delta, dq, heads, c_log2, scale, plan, n_qtiles, l0, l1, l2, l3, stash);
+  }
 }
 
 // ---- dK or dV: key-stationary -----------------------------------------------------------
@@ -402,20 +529,18 @@ struct KeyUnits {
 };
 
 // kMode: 0 = dV only, 1 = dK only, 2 = both in one pass (d = 64, where the
-// registers allow it)
-template <int D, int kMode>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout,
-                    const float* __restrict__ lse, const float* __restrict__ delta,
-                    __bf16* __restrict__ dk_chunks, __bf16* __restrict__ dk_anchor,
-                    __bf16* __restrict__ dv_chunks, __bf16* __restrict__ dv_anchor, int heads,
-                    float c_log2, float scale, PackedPlan plan, KeyUnits ku) {
+// registers allow it).  Slot = Q tile, dO tile, their log-sum-exp and D.
+template <int D, int kMode, int NS>
+__device__ __attribute__((always_inline)) inline void dkv_body(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ dout, const float* __restrict__ lse,
+    const float* __restrict__ delta, __bf16* __restrict__ dk_chunks, __bf16* __restrict__ dk_anchor,
+    __bf16* __restrict__ dv_chunks, __bf16* __restrict__ dv_anchor, int heads, float c_log2,
+    float scale, const PackedPlan& plan, const KeyUnits& ku, char* s0, char* s1, char* s2, char* s3,
+    char* stash) {
   constexpr bool kDK = kMode != 0;   // dK (needs dP)
   constexpr bool kDV = kMode != 1;
   using C = Cfg<D>;
-  __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
-  __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
-  __shared__ __attribute__((aligned(1024))) char stash[kDK ? kBlockN * C::ROWB : 16];
+  using R = Ring<NS>;
   const int nq = plan.chunk_tokens, G = plan.frame_tokens;
   const int n_units = plan.n_chunks * ku.kpc + ku.n_frames * ku.kpf;
   const int logical = xcd_logical(blockIdx.x, gridDim.x);
@@ -463,7 +588,7 @@ void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dou
   }
 
   // query runs of this unit
-  Stream<D, true> st;
+  Stream<D, true, R::kCopyWaves> st;
   st.wave = wave;
   st.lane = lane;
   st.row_bytes = uint32_t(2 * row_elems);
@@ -492,78 +617,91 @@ void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dou
   }
   st.n_tiles = 0;
   for (int i = 0; i < st.n_runs; ++i) st.n_tiles += (st.run_len(i) + kBT - 1) / kBT;
-#pragma unroll
-  for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
-    const int r = (wave * C::BLOCKS_PER_WAVE + i) * C::RPB + lane / C::CPR;
-    st.cp_row[i] = r;
-    st.cp_choff[i] = 16 * ((lane % C::CPR) ^ swz<D>(r));
-  }
+  st.init_copy_lanes();
   Lanes<D> ln(lane);
-  int csg = 0, ck0 = 0;
+  int csg = 0, ck0 = 0;   // next tile this wave works on
 
-  auto tile = [&](int t, char* cur, char* nxt) __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (t + 1 < st.n_tiles) st.issue(nxt);
+  auto issue = [&](char* slot) __attribute__((always_inline)) { st.issue(slot); };
+  auto next_nv = [&]() __attribute__((always_inline)) {
+    const int nv = min(kBT, st.run_len(csg) - ck0);
+    st.advance(csg, ck0);
+    return nv;
+  };
+  auto block = [&](const char* cur, int kb, int nv) __attribute__((always_inline)) {
     // keep the per-read address arithmetic inside the loop (no hoisted copies)
     asm volatile("" : "+v"(ln.a_lane), "+v"(ln.t_lane[0]), "+v"(ln.t_lane[1]));
-    const int nv = min(kBT, st.run_len(csg) - ck0);
     const float* lse_t = reinterpret_cast<const float*>(cur + 2 * C::TILE);
     const float* del_t = reinterpret_cast<const float*>(cur + 2 * C::TILE + C::VEC);
+    f32x16 sv;
+    rows_times_b<D>(cur, kb, ln.a_lane, kreg, sv);                // S = Q K^T (rows = queries)
+    __builtin_amdgcn_sched_barrier(0);
+    f32x16 dp;
+    if constexpr (kDK) rows_times_stash<D>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);   // dP = dO V^T
+    __builtin_amdgcn_sched_barrier(0);
+    uint32_t pk[8], pv[8];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x16 s;
-      rows_times_b<D>(cur, kb, ln.a_lane, kreg, s);               // S = Q K^T (rows = queries)
-      __builtin_amdgcn_sched_barrier(0);
-      f32x16 dp;
-      if constexpr (kDK) rows_times_stash<D>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);   // dP = dO V^T
-      __builtin_amdgcn_sched_barrier(0);
-      uint32_t pk[8], pv[8];
+    for (int g = 0; g < 4; ++g) {
+      const int r0 = kb * 32 + 8 * g + 4 * half;
+      const f32x4 Lr = *reinterpret_cast<const f32x4*>(lse_t + r0);
+      f32x4 Dr;
+      if constexpr (kDK) Dr = *reinterpret_cast<const f32x4*>(del_t + r0);
+      float v4[4], p4[4];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int r0 = kb * 32 + 8 * g + 4 * half;
-        const f32x4 Lr = *reinterpret_cast<const f32x4*>(lse_t + r0);
-        f32x4 Dr;
-        if constexpr (kDK) Dr = *reinterpret_cast<const f32x4*>(del_t + r0);
-        float v4[4], p4[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float p = r0 + e < nv ? __builtin_amdgcn_exp2f(fmaf(s[4 * g + e], c_log2, -Lr[e])) : 0.0f;
-          p4[e] = p;
-          if constexpr (kDK) v4[e] = p * (dp[4 * g + e] - Dr[e]);
-        }
-        if constexpr (kDK) {
-          pk[2 * g] = pack_bf16(v4[0], v4[1]);
-          pk[2 * g + 1] = pack_bf16(v4[2], v4[3]);
-        }
-        if constexpr (kDV) {
-          pv[2 * g] = pack_bf16(p4[0], p4[1]);
-          pv[2 * g + 1] = pack_bf16(p4[2], p4[3]);
-        }
+      for (int e = 0; e < 4; ++e) {
+        const float p = r0 + e < nv ? __builtin_amdgcn_exp2f(fmaf(sv[4 * g + e], c_log2, -Lr[e])) : 0.0f;
+        p4[e] = p;
+        if constexpr (kDK) v4[e] = p * (dp[4 * g + e] - Dr[e]);
       }
-      // dV^T += dO^T P, dK^T += Q^T dS
-      if constexpr (kMode == 0) rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc);
-      if constexpr (kMode == 1) rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);
-      if constexpr (kMode == 2) {
-        rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc_v);
-        rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);
+      if constexpr (kDK) {
+        pk[2 * g] = pack_bf16(v4[0], v4[1]);
+        pk[2 * g + 1] = pack_bf16(v4[2], v4[3]);
       }
-      __builtin_amdgcn_sched_barrier(0);   // one 32-query block at a time (register budget)
+      if constexpr (kDV) {
+        pv[2 * g] = pack_bf16(p4[0], p4[1]);
+        pv[2 * g + 1] = pack_bf16(p4[2], p4[3]);
+      }
     }
-    st.advance(csg, ck0);
+    // dV^T += dO^T P, dK^T += Q^T dS
+    if constexpr (kMode == 0) rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc);
+    if constexpr (kMode == 1) rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);
+    if constexpr (kMode == 2) {
+      rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc_v);
+      rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);
+    }
+    __builtin_amdgcn_sched_barrier(0);   // one 32-query block at a time (register budget)
   };
-  if (st.n_tiles > 0) st.issue(lds0);
-  for (int t = 0; t < st.n_tiles;) {
-    tile(t, lds0, lds1);
-    if (++t >= st.n_tiles) break;
-    tile(t, lds1, lds0);
-    ++t;
-  }
+  if (st.n_tiles > 0) run_ring<NS>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv, block);
   if constexpr (kMode == 0) store_t<D>(obase_v + head * D, row_elems, k0 + l32, n_keys, lane, acc, 1.0f);
   if constexpr (kMode == 1) store_t<D>(obase_k + head * D, row_elems, k0 + l32, n_keys, lane, acc, scale);
   if constexpr (kMode == 2) {
     store_t<D>(obase_k + head * D, row_elems, k0 + l32, n_keys, lane, acc, scale);
     store_t<D>(obase_v + head * D, row_elems, k0 + l32, n_keys, lane, acc_v, 1.0f);
+  }
+}
+
+template <int D, int kMode, int NS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout,
+                    const float* __restrict__ lse, const float* __restrict__ delta,
+                    __bf16* __restrict__ dk_chunks, __bf16* __restrict__ dk_anchor,
+                    __bf16* __restrict__ dv_chunks, __bf16* __restrict__ dv_anchor, int heads,
+                    float c_log2, float scale, PackedPlan plan, KeyUnits ku) {
+  constexpr int kSlot = 2 * Cfg<D>::TILE + 2 * Cfg<D>::VEC;
+  __shared__ __attribute__((aligned(1024))) char stash[kMode != 0 ? kBlockN * Cfg<D>::ROWB : 16];
+  __shared__ __attribute__((aligned(1024))) char l0[kSlot];
+  __shared__ __attribute__((aligned(1024))) char l1[kSlot];
+  if constexpr (NS == 2) {
+    dkv_body<D, kMode, NS>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
+                           c_log2, scale, plan, ku, l0, l1, l1, l1, stash);
+  } else if constexpr (NS == 3) {
+    __shared__ __attribute__((aligned(1024))) char l2[kSlot];
+    dkv_body<D, kMode, NS>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
+                           c_log2, scale, plan, ku, l0, l1, l2, l2, stash);
+  } else {
+    __shared__ __attribute__((aligned(1024))) char l2[kSlot];
+    __shared__ __attribute__((aligned(1024))) char l3[kSlot];
+    dkv_body<D, kMode, NS>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
+                           c_log2, scale, plan, ku, l0, l1, l2, l3, stash);
   }
 }
 
@@ -595,20 +733,23 @@ hipError_t launch_attention_bwd_bf16(const void* q, const void* out, const void*
   const __bf16* dp = static_cast<const __bf16*>(dout);
   __bf16 *dkp = static_cast<__bf16*>(dk), *dvp = static_cast<__bf16*>(dv);
   __bf16 *dakp = static_cast<__bf16*>(dak), *davp = static_cast<__bf16*>(dav);
-  // dV and dK in separate passes: one fused pass needs both accumulators at once,
-  // more registers than two waves per SIMD leave
+  // Rings (LDS: 160 KB per workgroup): d = 128 dQ fits three 32 KB slots beside its 64 KB
+  // dO stash, dV four 33 KB slots, dK (stash plus the streamed vectors) only two;
+  // d = 64 takes four everywhere.  dV and dK run as separate passes at d = 128:
+  // one fused pass needs both accumulators at once, more registers than two
+  // waves per SIMD leave.
   if (head_dim == 128) {
-    hipLaunchKernelGGL(bwd_dq_kernel<128>, g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
+    hipLaunchKernelGGL((bwd_dq_kernel<128, 3>), g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
                        static_cast<__bf16*>(dq), heads, c_log2, softmax_scale, plan, n_qtiles);
-    hipLaunchKernelGGL((bwd_dkv_kernel<128, 0>), g_k, dim3(kThreads), 0, stream, qp, dp, lse, delta,
-                       dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
-    hipLaunchKernelGGL((bwd_dkv_kernel<128, 1>), g_k, dim3(kThreads), 0, stream, qp, dp, lse, delta,
-                       dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
+    hipLaunchKernelGGL((bwd_dkv_kernel<128, 0, 4>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+                       delta, dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
+    hipLaunchKernelGGL((bwd_dkv_kernel<128, 1, 2>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+                       delta, dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
   } else {
-    hipLaunchKernelGGL(bwd_dq_kernel<64>, g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
+    hipLaunchKernelGGL((bwd_dq_kernel<64, 4>), g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
                        static_cast<__bf16*>(dq), heads, c_log2, softmax_scale, plan, n_qtiles);
-    hipLaunchKernelGGL((bwd_dkv_kernel<64, 2>), g_k, dim3(kThreads), 0, stream, qp, dp, lse, delta,
-                       dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
+    hipLaunchKernelGGL((bwd_dkv_kernel<64, 2, 4>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+                       delta, dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
   }
   return hipGetLastError();
 }
