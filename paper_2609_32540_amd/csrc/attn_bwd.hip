@@ -16,10 +16,13 @@
 //
 // Products on v_mfma_f32_32x32x16_bf16 with the forward's operand layouts: the
 // stationary side (Q^T and dO^T, or K^T and V^T) sits in registers as the B
-// operand, tiles of the streamed side are copied HBM -> LDS (global_load_lds)
-// one tile ahead into a two-slot ring and read as the A operand (16-byte rows)
-// or, transposed, with ds_read_b64_tr_b16; P and dS go from the accumulators to
-// the B operand of the next product as bf16 (nearest even).
+// operand (the second one, where registers run out, in a swizzled LDS copy),
+// tiles of the streamed side are copied HBM -> LDS (global_load_lds) ahead of
+// use into a ring of two to four slots and read as the A operand (16-byte
+// rows) or, transposed, with ds_read_b64_tr_b16; P and dS go from the
+// accumulators to the B operand of the next product as bf16 (nearest even).
+// With three or more slots the two waves of each SIMD work half a tile apart,
+// as in the forward kernel (see Ring).
 
 #include <hip/hip_runtime.h>
 
