@@ -50,20 +50,20 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBlockN = 32 * kWaves;   // stationary columns (queries or keys) per workgroup
-constexpr int kBT = 64;                // streamed rows per tile
+constexpr int kBT = 64;                // streamed rows per tile (32 for the d = 128 dK pass)
 constexpr int kXcds = 8;
 constexpr int kMaxRuns = 2 * FF_MAX_ANCHOR_FRAMES + 1;   // segments of one streamed set
 
-template <int D>
+template <int D, int BT = kBT>
 struct Cfg {
   static constexpr int KS = D / 16;
   static constexpr int DB = D / 32;
   static constexpr int ROWB = 2 * D;
   static constexpr int CPR = D / 8;
   static constexpr int RPB = 1024 / ROWB;
-  static constexpr int BLOCKS = kBT / RPB;              // 1 KB copies per tile and tensor
-  static constexpr int TILE = kBT * ROWB;
-  static constexpr int VEC = kBT * 4;                   // one float per streamed row
+  static constexpr int BLOCKS = BT / RPB;               // 1 KB copies per tile and tensor
+  static constexpr int TILE = BT * ROWB;
+  static constexpr int VEC = BT * 4;                    // one float per streamed row
   static_assert(BLOCKS % kWaves == 0, "every wave copies the same number of 1 KB blocks");
 };
 
@@ -105,9 +105,9 @@ __device__ inline uint64_t readlane_u64(uint64_t v, int lane) {
 // token-major tensors (row r at a + r * row_bytes and b + r * row_bytes, this
 // head's columns) and, with kVec, two float vectors (element r at
 // va + r * vec_bytes and vb + r * vec_bytes).
-template <int D, bool kVec, int kCopyWaves>
+template <int D, bool kVec, int kCopyWaves, int BT = kBT>
 struct Stream {
-  using C = Cfg<D>;
+  using C = Cfg<D, BT>;
   static constexpr int BPW = C::BLOCKS / kCopyWaves;   // 1 KB blocks per copying wave and tensor
   int len = 0;
   uint64_t a = 0, b = 0, va = 0, vb = 0;
@@ -128,7 +128,7 @@ struct Stream {
 
   __device__ int run_len(int i) const { return __builtin_amdgcn_readlane(len, i); }
   __device__ void advance(int& s, int& k) const {
-    k += kBT;
+    k += BT;
     if (k >= run_len(s)) {
       ++s;
       k = 0;
@@ -140,7 +140,7 @@ struct Stream {
     const int n = run_len(sg);
     const char* ga = reinterpret_cast<const char*>(readlane_u64(a, sg));
     const char* gb = reinterpret_cast<const char*>(readlane_u64(b, sg));
-    const bool partial = k0 + kBT > n;
+    const bool partial = k0 + BT > n;
 #pragma unroll
     for (int i = 0; i < BPW; ++i) {
       int tok = k0 + cp_row[i];
@@ -151,7 +151,7 @@ struct Stream {
       __builtin_amdgcn_global_load_lds(GLOBAL_PTR(gb + off), LDS_PTR(void, dst + C::TILE), 16, 0, 0);
     }
     if constexpr (kVec) {
-      if (wave == 0) {
+      if (wave == 0 && lane < BT) {   // one float per row: lanes 0 .. BT-1
         const char* pa = reinterpret_cast<const char*>(readlane_u64(va, sg));
         const char* pb = reinterpret_cast<const char*>(readlane_u64(vb, sg));
         const uint32_t off = uint32_t(min(k0 + lane, n - 1)) * vec_bytes;
@@ -163,14 +163,15 @@ struct Stream {
   }
 };
 
-// Drives the tile loop of one workgroup over n > 0 tiles with the Ring<NS>
-// schedule.  issue(slot) copies the stream's next tile into slot (copy waves
-// only); next_nv() returns the valid rows of the next tile this wave works on
-// and advances its cursor; block(slot, kb, nv) works on 32-row block kb of
-// the tile in slot.  Slots are distinct __shared__ arrays, referenced
+// Drives the tile loop of one workgroup over n > 0 tiles of kBlocks 32-row
+// blocks with the Ring<NS> schedule.  issue(slot) copies the stream's next
+// tile into slot (copy waves only); next_nv() returns the valid rows of the
+// next tile this wave works on and advances its cursor; block(slot, kb, nv)
+// works on block kb of the tile in slot.  With one block per tile, waves 4-7
+// work on tile t-1 while waves 0-3 work on tile t.  Slots are distinct __shared__ arrays, referenced
 // statically (the loops are unrolled by NS), so the compiler never orders a
 // read of one slot behind a copy into another.
-template <int NS, class Issue, class NextNv, class Block>
+template <int NS, int kBlocks, class Issue, class NextNv, class Block>
 __device__ __attribute__((always_inline)) inline void run_ring(int n, int wave, char* s0, char* s1,
                                                                char* s2, char* s3, Issue& issue,
                                                                NextNv& next_nv, Block& block) {
@@ -186,7 +187,7 @@ __device__ __attribute__((always_inline)) inline void run_ring(int n, int wave, 
       if (t + 1 < n) issue(nxt);
       const int nv = next_nv();
       block(cur, 0, nv);
-      block(cur, 1, nv);
+      if constexpr (kBlocks == 2) block(cur, 1, nv);
     };
     for (int t = 0; t < n;) {
       step(t, s0, s1);
@@ -202,7 +203,7 @@ __device__ __attribute__((always_inline)) inline void run_ring(int n, int wave, 
       if (t + R::kAhead < n) issue(ahead);
       const int nv = next_nv();
       block(cur, 0, nv);
-      block(cur, 1, nv);
+      if constexpr (kBlocks == 2) block(cur, 1, nv);
     };
     for (int t = 0; t < n;) {
       if constexpr (NS == 3) {
@@ -224,6 +225,32 @@ __device__ __attribute__((always_inline)) inline void run_ring(int n, int wave, 
       }
     }
     sync();   // matches the extra barrier of waves 4-7
+  } else if constexpr (kBlocks == 1) {
+    sync();
+    // step t: barrier t, tile t-1
+    auto step = [&](int t, char* prev) __attribute__((always_inline)) {
+      sync();
+      block(prev, 0, next_nv());
+    };
+    for (int t = 1;;) {
+      if constexpr (NS == 3) {
+        step(t, s0);
+        if (t++ >= n) break;
+        step(t, s1);
+        if (t++ >= n) break;
+        step(t, s2);
+        if (t++ >= n) break;
+      } else {
+        step(t, s0);
+        if (t++ >= n) break;
+        step(t, s1);
+        if (t++ >= n) break;
+        step(t, s2);
+        if (t++ >= n) break;
+        step(t, s3);
+        if (t++ >= n) break;
+      }
+    }
   } else {
     sync();
     int nv_prev = next_nv();
@@ -495,7 +522,7 @@ __device__ __attribute__((always_inline)) inline void dq_body(
     rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);                     // dQ^T += K^T dS^T
     __builtin_amdgcn_sched_barrier(0);   // one 32-key block at a time (register budget)
   };
-  if (st.n_tiles > 0) run_ring<NS>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv, block);
+  if (st.n_tiles > 0) run_ring<NS, 2>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv, block);
   store_t<D>(dq + tok0 * row_elems + head * D, row_elems, q0 + l32, nq, lane, acc, scale);
 }
 
@@ -533,7 +560,7 @@ struct KeyUnits {
 
 // kMode: 0 = dV only, 1 = dK only, 2 = both in one pass (d = 64, where the
 // registers allow it).  Slot = Q tile, dO tile, their log-sum-exp and D.
-template <int D, int kMode, int NS>
+template <int D, int kMode, int NS, int BT>
 __device__ __attribute__((always_inline)) inline void dkv_body(
     const __bf16* __restrict__ q, const __bf16* __restrict__ dout, const float* __restrict__ lse,
     const float* __restrict__ delta, __bf16* __restrict__ dk_chunks, __bf16* __restrict__ dk_anchor,
@@ -542,8 +569,9 @@ __device__ __attribute__((always_inline)) inline void dkv_body(
     char* stash) {
   constexpr bool kDK = kMode != 0;   // dK (needs dP)
   constexpr bool kDV = kMode != 1;
-  using C = Cfg<D>;
+  using C = Cfg<D, BT>;
   using R = Ring<NS>;
+  constexpr int kBlocks = BT / 32;
   const int nq = plan.chunk_tokens, G = plan.frame_tokens;
   const int n_units = plan.n_chunks * ku.kpc + ku.n_frames * ku.kpf;
   const int logical = xcd_logical(blockIdx.x, gridDim.x);
@@ -591,7 +619,7 @@ __device__ __attribute__((always_inline)) inline void dkv_body(
   }
 
   // query runs of this unit
-  Stream<D, true, R::kCopyWaves> st;
+  Stream<D, true, R::kCopyWaves, BT> st;
   st.wave = wave;
   st.lane = lane;
   st.row_bytes = uint32_t(2 * row_elems);
@@ -619,14 +647,14 @@ __device__ __attribute__((always_inline)) inline void dkv_body(
     st.n_runs = n;
   }
   st.n_tiles = 0;
-  for (int i = 0; i < st.n_runs; ++i) st.n_tiles += (st.run_len(i) + kBT - 1) / kBT;
+  for (int i = 0; i < st.n_runs; ++i) st.n_tiles += (st.run_len(i) + BT - 1) / BT;
   st.init_copy_lanes();
   Lanes<D> ln(lane);
   int csg = 0, ck0 = 0;   // next tile this wave works on
 
   auto issue = [&](char* slot) __attribute__((always_inline)) { st.issue(slot); };
   auto next_nv = [&]() __attribute__((always_inline)) {
-    const int nv = min(kBT, st.run_len(csg) - ck0);
+    const int nv = min(BT, st.run_len(csg) - ck0);
     st.advance(csg, ck0);
     return nv;
   };
@@ -673,7 +701,7 @@ __device__ __attribute__((always_inline)) inline void dkv_body(
     }
     __builtin_amdgcn_sched_barrier(0);   // one 32-query block at a time (register budget)
   };
-  if (st.n_tiles > 0) run_ring<NS>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv, block);
+  if (st.n_tiles > 0) run_ring<NS, kBlocks>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv, block);
   if constexpr (kMode == 0) store_t<D>(obase_v + head * D, row_elems, k0 + l32, n_keys, lane, acc, 1.0f);
   if constexpr (kMode == 1) store_t<D>(obase_k + head * D, row_elems, k0 + l32, n_keys, lane, acc, scale);
   if constexpr (kMode == 2) {
@@ -682,28 +710,28 @@ __device__ __attribute__((always_inline)) inline void dkv_body(
   }
 }
 
-template <int D, int kMode, int NS>
+template <int D, int kMode, int NS, int BT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout,
                     const float* __restrict__ lse, const float* __restrict__ delta,
                     __bf16* __restrict__ dk_chunks, __bf16* __restrict__ dk_anchor,
                     __bf16* __restrict__ dv_chunks, __bf16* __restrict__ dv_anchor, int heads,
                     float c_log2, float scale, PackedPlan plan, KeyUnits ku) {
-  constexpr int kSlot = 2 * Cfg<D>::TILE + 2 * Cfg<D>::VEC;
+  constexpr int kSlot = 2 * Cfg<D, BT>::TILE + 2 * Cfg<D, BT>::VEC;
   __shared__ __attribute__((aligned(1024))) char stash[kMode != 0 ? kBlockN * Cfg<D>::ROWB : 16];
   __shared__ __attribute__((aligned(1024))) char l0[kSlot];
   __shared__ __attribute__((aligned(1024))) char l1[kSlot];
   if constexpr (NS == 2) {
-    dkv_body<D, kMode, NS>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
+    dkv_body<D, kMode, NS, BT>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
                            c_log2, scale, plan, ku, l0, l1, l1, l1, stash);
   } else if constexpr (NS == 3) {
     __shared__ __attribute__((aligned(1024))) char l2[kSlot];
-    dkv_body<D, kMode, NS>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
+    dkv_body<D, kMode, NS, BT>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
                            c_log2, scale, plan, ku, l0, l1, l2, l2, stash);
   } else {
     __shared__ __attribute__((aligned(1024))) char l2[kSlot];
     __shared__ __attribute__((aligned(1024))) char l3[kSlot];
-    dkv_body<D, kMode, NS>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
+    dkv_body<D, kMode, NS, BT>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
                            c_log2, scale, plan, ku, l0, l1, l2, l3, stash);
   }
 }
@@ -737,21 +765,21 @@ hipError_t launch_attention_bwd_bf16(const void* q, const void* out, const void*
   __bf16 *dkp = static_cast<__bf16*>(dk), *dvp = static_cast<__bf16*>(dv);
   __bf16 *dakp = static_cast<__bf16*>(dak), *davp = static_cast<__bf16*>(dav);
   // Rings (LDS: 160 KB per workgroup): d = 128 dQ fits three 32 KB slots beside its 64 KB
-  // dO stash, dV four 33 KB slots, dK (stash plus the streamed vectors) only two;
-  // d = 64 takes four everywhere.  dV and dK run as separate passes at d = 128:
+  // dO stash, dV four 33 KB slots, dK (stash plus the streamed vectors) four slots of
+  // 32-row tiles; d = 64 takes four 64-row slots everywhere.  dV and dK run as separate passes at d = 128:
   // one fused pass needs both accumulators at once, more registers than two
   // waves per SIMD leave.
   if (head_dim == 128) {
     hipLaunchKernelGGL((bwd_dq_kernel<128, 3>), g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
                        static_cast<__bf16*>(dq), heads, c_log2, softmax_scale, plan, n_qtiles);
-    hipLaunchKernelGGL((bwd_dkv_kernel<128, 0, 4>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+    hipLaunchKernelGGL((bwd_dkv_kernel<128, 0, 4, 64>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
                        delta, dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
-    hipLaunchKernelGGL((bwd_dkv_kernel<128, 1, 2>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+    hipLaunchKernelGGL((bwd_dkv_kernel<128, 1, 4, 32>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
                        delta, dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
   } else {
     hipLaunchKernelGGL((bwd_dq_kernel<64, 4>), g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
                        static_cast<__bf16*>(dq), heads, c_log2, softmax_scale, plan, n_qtiles);
-    hipLaunchKernelGGL((bwd_dkv_kernel<64, 2, 4>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+    hipLaunchKernelGGL((bwd_dkv_kernel<64, 2, 4, 64>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
                        delta, dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
   }
   return hipGetLastError();
