@@ -7,12 +7,12 @@
 //   dS_ij = P_ij (dO_i . v_j - D_i)
 //   dQ_i  = scale sum_j dS_ij k_j
 //   dK_j  = scale sum_i dS_ij q_i
-// Four launches: D; dQ (query-stationary: a workgroup holds 256 queries of one
-// chunk and head and streams the 64-key tiles of their read set, like the
-// forward); dV and dK (key-stationary: a workgroup holds 256 keys of one chunk
-// or anchor frame and head and streams the 64-query tiles of every chunk that
-// sees them).  Every output element is written by exactly one workgroup: no
-// atomics.
+// Three launches: D; dQ (query-stationary: a workgroup holds 256 queries of
+// one chunk and head and streams the 64-key tiles of their read set, like the
+// forward); dK and dV together (key-stationary: a workgroup holds 256 keys of
+// one chunk or anchor frame and head and streams the query tiles of every
+// chunk that sees them, 32 rows per tile at d = 128, 64 at d = 64).  Every
+// output element is written by exactly one workgroup: no atomics.
 //
 // Products on v_mfma_f32_32x32x16_bf16 with the forward's operand layouts: the
 // stationary side (Q^T and dO^T, or K^T and V^T) sits in registers as the B
@@ -558,17 +558,14 @@ struct KeyUnits {
   uint8_t frame_runs[FF_MAX_ANCHOR_FRAMES * 8][16];   // per anchor frame: (first chunk, count) pairs
 };
 
-// kMode: 0 = dV only, 1 = dK only, 2 = both in one pass (d = 64, where the
-// registers allow it).  Slot = Q tile, dO tile, their log-sum-exp and D.
-template <int D, int kMode, int NS, int BT>
+// dK and dV of one key unit.  Slot = Q tile, dO tile, their log-sum-exp and D.
+template <int D, int NS, int BT>
 __device__ __attribute__((always_inline)) inline void dkv_body(
     const __bf16* __restrict__ q, const __bf16* __restrict__ dout, const float* __restrict__ lse,
     const float* __restrict__ delta, __bf16* __restrict__ dk_chunks, __bf16* __restrict__ dk_anchor,
     __bf16* __restrict__ dv_chunks, __bf16* __restrict__ dv_anchor, int heads, float c_log2,
     float scale, const PackedPlan& plan, const KeyUnits& ku, char* s0, char* s1, char* s2, char* s3,
     char* stash) {
-  constexpr bool kDK = kMode != 0;   // dK (needs dP)
-  constexpr bool kDV = kMode != 1;
   using C = Cfg<D, BT>;
   using R = Ring<NS>;
   constexpr int kBlocks = BT / 32;
@@ -604,19 +601,16 @@ __device__ __attribute__((always_inline)) inline void dkv_body(
   const int k0 = k_first + wave * 32;
   bf16x8 kreg[C::KS];
   load_b<D>(kbase + head * D, row_elems, k0, n_keys, lane, kreg);
-  if constexpr (kDK) stash_b<D>(stash, vbase + head * D, row_elems, k0, n_keys, wave, lane);
-  const char* stash_w = stash + (kDK ? 32 * wave * C::ROWB : 0);
-  f32x16 acc[C::DB], acc_v[kMode == 2 ? C::DB : 1];
+  stash_b<D>(stash, vbase + head * D, row_elems, k0, n_keys, wave, lane);
+  const char* stash_w = stash + 32 * wave * C::ROWB;
+  f32x16 acc[C::DB], acc_v[C::DB];   // dK^T, dV^T
 #pragma unroll
   for (int db = 0; db < C::DB; ++db)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) acc[db][j] = 0.0f;
-  if constexpr (kMode == 2) {
-#pragma unroll
-    for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) acc_v[db][j] = 0.0f;
-  }
+    for (int j = 0; j < 16; ++j) {
+      acc[db][j] = 0.0f;
+      acc_v[db][j] = 0.0f;
+    }
 
   // query runs of this unit
   Stream<D, true, R::kCopyWaves, BT> st;
@@ -667,50 +661,37 @@ __device__ __attribute__((always_inline)) inline void dkv_body(
     rows_times_b<D>(cur, kb, ln.a_lane, kreg, sv);                // S = Q K^T (rows = queries)
     __builtin_amdgcn_sched_barrier(0);
     f32x16 dp;
-    if constexpr (kDK) rows_times_stash<D>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);   // dP = dO V^T
+    rows_times_stash<D>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);   // dP = dO V^T
     __builtin_amdgcn_sched_barrier(0);
     uint32_t pk[8], pv[8];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const int r0 = kb * 32 + 8 * g + 4 * half;
       const f32x4 Lr = *reinterpret_cast<const f32x4*>(lse_t + r0);
-      f32x4 Dr;
-      if constexpr (kDK) Dr = *reinterpret_cast<const f32x4*>(del_t + r0);
+      const f32x4 Dr = *reinterpret_cast<const f32x4*>(del_t + r0);
       float v4[4], p4[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float p = r0 + e < nv ? __builtin_amdgcn_exp2f(fmaf(sv[4 * g + e], c_log2, -Lr[e])) : 0.0f;
         p4[e] = p;
-        if constexpr (kDK) v4[e] = p * (dp[4 * g + e] - Dr[e]);
+        v4[e] = p * (dp[4 * g + e] - Dr[e]);
       }
-      if constexpr (kDK) {
-        pk[2 * g] = pack_bf16(v4[0], v4[1]);
-        pk[2 * g + 1] = pack_bf16(v4[2], v4[3]);
-      }
-      if constexpr (kDV) {
-        pv[2 * g] = pack_bf16(p4[0], p4[1]);
-        pv[2 * g + 1] = pack_bf16(p4[2], p4[3]);
-      }
+      pk[2 * g] = pack_bf16(v4[0], v4[1]);
+      pk[2 * g + 1] = pack_bf16(v4[2], v4[3]);
+      pv[2 * g] = pack_bf16(p4[0], p4[1]);
+      pv[2 * g + 1] = pack_bf16(p4[2], p4[3]);
     }
     // dV^T += dO^T P, dK^T += Q^T dS
-    if constexpr (kMode == 0) rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc);
-    if constexpr (kMode == 1) rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);
-    if constexpr (kMode == 2) {
-      rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc_v);
-      rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);
-    }
+    rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc_v);
+    rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);
     __builtin_amdgcn_sched_barrier(0);   // one 32-query block at a time (register budget)
   };
   if (st.n_tiles > 0) run_ring<NS, kBlocks>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv, block);
-  if constexpr (kMode == 0) store_t<D>(obase_v + head * D, row_elems, k0 + l32, n_keys, lane, acc, 1.0f);
-  if constexpr (kMode == 1) store_t<D>(obase_k + head * D, row_elems, k0 + l32, n_keys, lane, acc, scale);
-  if constexpr (kMode == 2) {
-    store_t<D>(obase_k + head * D, row_elems, k0 + l32, n_keys, lane, acc, scale);
-    store_t<D>(obase_v + head * D, row_elems, k0 + l32, n_keys, lane, acc_v, 1.0f);
-  }
+  store_t<D>(obase_k + head * D, row_elems, k0 + l32, n_keys, lane, acc, scale);
+  store_t<D>(obase_v + head * D, row_elems, k0 + l32, n_keys, lane, acc_v, 1.0f);
 }
 
-template <int D, int kMode, int NS, int BT>
+template <int D, int NS, int BT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dout,
                     const float* __restrict__ lse, const float* __restrict__ delta,
@@ -718,20 +699,20 @@ void bwd_dkv_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ dou
                     __bf16* __restrict__ dv_chunks, __bf16* __restrict__ dv_anchor, int heads,
                     float c_log2, float scale, PackedPlan plan, KeyUnits ku) {
   constexpr int kSlot = 2 * Cfg<D, BT>::TILE + 2 * Cfg<D, BT>::VEC;
-  __shared__ __attribute__((aligned(1024))) char stash[kMode != 0 ? kBlockN * Cfg<D>::ROWB : 16];
+  __shared__ __attribute__((aligned(1024))) char stash[kBlockN * Cfg<D>::ROWB];
   __shared__ __attribute__((aligned(1024))) char l0[kSlot];
   __shared__ __attribute__((aligned(1024))) char l1[kSlot];
   if constexpr (NS == 2) {
-    dkv_body<D, kMode, NS, BT>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
+    dkv_body<D, NS, BT>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
                            c_log2, scale, plan, ku, l0, l1, l1, l1, stash);
   } else if constexpr (NS == 3) {
     __shared__ __attribute__((aligned(1024))) char l2[kSlot];
-    dkv_body<D, kMode, NS, BT>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
+    dkv_body<D, NS, BT>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
                            c_log2, scale, plan, ku, l0, l1, l2, l2, stash);
   } else {
     __shared__ __attribute__((aligned(1024))) char l2[kSlot];
     __shared__ __attribute__((aligned(1024))) char l3[kSlot];
-    dkv_body<D, kMode, NS, BT>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
+    dkv_body<D, NS, BT>(q, dout, lse, delta, dk_chunks, dk_anchor, dv_chunks, dv_anchor, heads,
                            c_log2, scale, plan, ku, l0, l1, l2, l3, stash);
   }
 }
@@ -765,21 +746,18 @@ hipError_t launch_attention_bwd_bf16(const void* q, const void* out, const void*
   __bf16 *dkp = static_cast<__bf16*>(dk), *dvp = static_cast<__bf16*>(dv);
   __bf16 *dakp = static_cast<__bf16*>(dak), *davp = static_cast<__bf16*>(dav);
   // Rings (LDS: 160 KB per workgroup): d = 128 dQ fits three 32 KB slots beside its 64 KB
-  // dO stash, dV four 33 KB slots, dK (stash plus the streamed vectors) four slots of
-  // 32-row tiles; d = 64 takes four 64-row slots everywhere.  dV and dK run as separate passes at d = 128:
-  // one fused pass needs both accumulators at once, more registers than two
-  // waves per SIMD leave.
+  // dO stash; the d = 128 dK/dV pass (V stash plus the streamed vectors) four slots of
+  // 32-row tiles, which also keeps the per-block registers within two waves per SIMD
+  // beside both accumulators; d = 64 takes four 64-row slots in both passes.
   if (head_dim == 128) {
     hipLaunchKernelGGL((bwd_dq_kernel<128, 3>), g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
                        static_cast<__bf16*>(dq), heads, c_log2, softmax_scale, plan, n_qtiles);
-    hipLaunchKernelGGL((bwd_dkv_kernel<128, 0, 4, 64>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
-                       delta, dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
-    hipLaunchKernelGGL((bwd_dkv_kernel<128, 1, 4, 32>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+    hipLaunchKernelGGL((bwd_dkv_kernel<128, 4, 32>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
                        delta, dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
   } else {
     hipLaunchKernelGGL((bwd_dq_kernel<64, 4>), g_q, dim3(kThreads), 0, stream, qp, dp, lse, delta,
                        static_cast<__bf16*>(dq), heads, c_log2, softmax_scale, plan, n_qtiles);
-    hipLaunchKernelGGL((bwd_dkv_kernel<64, 2, 4, 64>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
+    hipLaunchKernelGGL((bwd_dkv_kernel<64, 4, 64>), g_k, dim3(kThreads), 0, stream, qp, dp, lse,
                        delta, dkp, dakp, dvp, davp, heads, c_log2, softmax_scale, plan, ku);
   }
   return hipGetLastError();
