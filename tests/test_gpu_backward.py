@@ -87,6 +87,14 @@ def test_backward_small(d, W):
     run_case(6, 198, 66, 3, TABLE6, W, 2, d)
 
 
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("W", [0, 1])
+def test_backward_one_and_two_tile_streams(d, W):
+    # 20-token chunks and 10-token frames: every workgroup streams one to
+    # three partial tiles, so the ring schedules run their shortest loops
+    run_case(3, 20, 10, 2, [[0], [], [0, 1]], W, 3, d, seed=11)
+
+
 def test_backward_multi_tile_and_hidden_frame():
     # 288-token chunks (4.5 tiles), 96-token frames, a frame no chunk lists, 4 heads
     table = [[0], [0, 1], [1], [1, 3], [3], [3]]
