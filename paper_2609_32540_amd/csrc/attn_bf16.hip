@@ -41,7 +41,9 @@
 // conflicts on the 64-bank LDS.
 // Workgroups are renumbered so that consecutive Q tiles of one head land on
 // the same XCD (the hardware deals workgroups to the 8 XCDs round robin) and
-// share that XCD's L2 for the head's K/V.
+// share that XCD's L2 for the head's K/V.  When the units do not fill the last
+// round of the GPU, the host splits that round's units along their keys into
+// up to four parts (unnormalised fp32 partials, merged by tail_merge_kernel).
 
 #include <hip/hip_runtime.h>
 
@@ -147,10 +149,10 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   __shared__ __attribute__((aligned(1024))) char lds2[C::SLOT];
   __shared__ __attribute__((aligned(1024))) char lds3[C::SLOT];
 
-  // XCD-aware renumbering: hardware block b runs on XCD b % 8; give each XCD a
-  // contiguous range of logical tiles.
-  // (the tail-round workgroups b >= tail.n_full take part tail.split of one
-  // unit's key tiles each)
+  // Workgroups b < tail.n_full run whole units (head, 256-query tile),
+  // renumbered XCD-aware: hardware block b runs on XCD b % 8, so each XCD gets
+  // a contiguous range of units.  The later ones run key part b % split of
+  // unit n_full + (b - n_full) / split (the partial last round, see TailSplit).
   const int b = blockIdx.x;
   int logical, part_id = 0, n_parts = 1;
   if (b < tail.n_full) {
