@@ -283,7 +283,8 @@ def wavefront_clip(name: str = "1.3b-480p") -> dict:
 
     one = [torch.cuda.Stream()]
     many = [torch.cuda.Stream() for _ in range(S)]
-    run(one)                                   # warm (allocator, code objects)
+    run(one)                                   # warm: code objects and each stream's
+    run(many)                                  # pool of the caching allocator
     t_seq, _, _, X_seq = run(one)
     t_wave, rounds, fwd, X_wave = run(many)
     same = all(torch.equal(a, b) for a, b in zip(X_seq, X_wave))
