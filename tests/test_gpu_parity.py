@@ -219,6 +219,39 @@ def test_attention_tail_split_into_key_parts(head_dim, grid):
         run.step(c, 0, 0)
 
 
+@pytest.mark.parametrize("dtype,head_dim,grid", [("bf16", 128, (3, 5)), ("bf16", 128, (6, 11)),
+                                                  ("bf16", 64, (6, 11)), ("f32", 64, (3, 5))])
+def test_attention_maximum_segments(dtype, head_dim, grid):
+    # the largest read set: 8 non-adjacent anchor frames of a 16-frame bank
+    # (8 runs), a full ring of W = 8 chunks (wrapped once) and the chunk: 17
+    # segments, each shorter than (3x5 grid) or not a multiple of one key tile
+    W = ff.MAX_RING_CHUNKS
+    w = small(dtype, head_dim, heads=3, grid_h=grid[0], grid_w=grid[1], ring_chunks=W,
+              stages=1, layers=1, n_chunks=W + 3, anchor_rule="none",
+              max_anchor_frames=ff.MAX_ANCHOR_FRAMES)
+    bank_frames = list(range(16))
+    bk, bv = synth.anchor_tensors(w, bank_frames, 0)
+    bkd, bvd = to_dev(bk), to_dev(bv)
+    window = [14, 0, 6, 2, 10, 4, 12, 8]            # listed out of order on purpose
+    assert len(window) == ff.MAX_ANCHOR_FRAMES
+    G = w.tokens_per_frame
+    cache = make_cache(w, 1, 1)
+    hist = []
+    for c in range(w.n_chunks):
+        q, k, v = (synth.chunk_tensor(w, t, c, 0, 0) for t in (synth.T_Q, synth.T_K, synth.T_V))
+        out = cache.chunk_attention_bank(0, 0, c, to_dev(q), to_dev(k), to_dev(v), bkd, bvd, window)
+        cache.kv_publish(0, 0, c, to_dev(k), to_dev(v))
+        keys = [exact(bk[f * G:(f + 1) * G]) for f in window] + [h[0] for h in hist] + [exact(k)]
+        vals = [exact(bv[f * G:(f + 1) * G]) for f in window] + [h[1] for h in hist] + [exact(v)]
+        K_all, V_all = np.concatenate(keys), np.concatenate(vals)
+        ref = fo.masked_attention(exact(q), K_all, V_all, np.ones(len(K_all), bool),
+                                  1.0 / math.sqrt(head_dim))
+        check_attention(exact(out), ref, dtype, f"chunk {c}")
+        hist = (hist + [(exact(k), exact(v))])[-W:]
+    table, count = cache.ring_state(0, 0)
+    assert count == w.n_chunks and sorted(table) == list(range(w.n_chunks - W, w.n_chunks))
+
+
 def test_unfilled_slots_poisoned_with_nan_are_never_read():
     w = small("bf16", 128, ring_chunks=4, anchor_rule="fixed:3", max_anchor_frames=3)
     run = PairedRun(w, poison=True)
