@@ -155,7 +155,20 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   // unit n_full + (b - n_full) / split (the partial last round, see TailSplit).
   const int b = blockIdx.x;
   int logical, part_id = 0, n_parts = 1;
-  if (b < tail.n_full) {
+  const int n_pairs = kPacked ? gridDim.x / n_qtiles : 0;      // (chunk, head) pairs
+  const int n_even = n_pairs - n_pairs % kXcds;
+  if (kPacked) {
+    // packed clip: the chunks' read sets differ in length, so XCD x takes the
+    // (chunk, head) pairs p = x, x + 8, .. (the q tiles of one pair stay on one
+    // XCD and share its L2): every XCD gets the same mix of chunks; the last
+    // n_pairs % 8 pairs run in order
+    if (b < n_even * n_qtiles) {
+      const int xcd = b % kXcds, idx = b / kXcds;
+      logical = (xcd + kXcds * (idx / n_qtiles)) * n_qtiles + idx % n_qtiles;
+    } else {
+      logical = b;
+    }
+  } else if (b < tail.n_full) {
     const int n_wg = tail.n_full;
     const int xcd = b % kXcds, idx = b / kXcds;
     const int per = n_wg / kXcds, rem = n_wg % kXcds;

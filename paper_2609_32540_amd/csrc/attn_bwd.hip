@@ -421,6 +421,18 @@ __device__ inline int xcd_logical(int b, int n_wg) {
   return xcd * per + min(xcd, rem) + idx;
 }
 
+// Groups of `group` consecutive logical units that share a read set (the q
+// tiles of one (chunk, head)) but cost differently from group to group: XCD x
+// takes the groups x, x + 8, .. so every XCD gets the same mix; the last
+// n_groups % 8 groups run in order.
+__device__ inline int xcd_interleaved(int b, int n_wg, int group) {
+  const int n_groups = n_wg / group;
+  const int n_even = n_groups - n_groups % kXcds;
+  if (b >= n_even * group) return b;
+  const int xcd = b % kXcds, idx = b / kXcds;
+  return (xcd + kXcds * (idx / group)) * group + idx % group;
+}
+
 // ---- D_i = dO_i . O_i ---------------------------------------------------------------
 __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict__ o,
                                                         const __bf16* __restrict__ dout,
@@ -452,7 +464,7 @@ __device__ __attribute__((always_inline)) inline void dq_body(
   using C = Cfg<D>;
   using R = Ring<NS>;
   const int nq = plan.chunk_tokens;
-  const int logical = xcd_logical(blockIdx.x, gridDim.x);
+  const int logical = xcd_interleaved(blockIdx.x, gridDim.x, n_qtiles);
   const int chunk = logical / (heads * n_qtiles);
   const int rest = logical - chunk * heads * n_qtiles;
   const int head = rest / n_qtiles, qt = rest % n_qtiles;
