@@ -2,8 +2,8 @@
 //
 // Work split: a workgroup = 8 waves = 256 queries of one head, one workgroup
 // per CU (two waves per SIMD); each wave owns 32 queries for the whole key
-// loop.  Keys
-// arrive as segments (anchor segment, valid history slots, current chunk);
+// loop.  Keys arrive as segments (anchor segment, valid history slots, current
+// chunk);
 // each segment is cut into 64-key tiles and only a segment's last tile is
 // partial (its missing keys are masked to -inf): no tile straddles two
 // segments and no empty slot is touched.
@@ -16,15 +16,17 @@
 //                   so max and sum are in-lane plus one v_permlane32_swap.  exp2
 //                   with log2(e) folded into the scale.  The running max is only
 //                   raised (and O rescaled) when a column max exceeds it by more
-//                   than 2^8; otherwise the stale max is kept, which leaves the
-//                   result exact since the final sum uses the same max.
+//                   than 8 (log2 units, probabilities up to 2^8); otherwise the
+//                   stale max stays the reference, which leaves the result exact
+//                   since the final sum uses the same max.
 //   O^T += V^T P^T  A = V^T, read from the row-major V tile with the gfx950
 //                   transposing LDS read (ds_read_b64_tr_b16); B = P^T, the
 //                   softmax registers rounded to bf16 in place.  The keys of each
 //                   8-key operand are chosen to match the accumulator layout.
-// Software pipeline: while the matrix core computes block 0 of S^T of tile
-// t+1, the VALU exponentiates tile t (h1); the products of tile t into O^T,
-// block 1 of S^T(t+1) and the column max of tile t+1 follow (h2).  Waves w and
+// Software pipeline: h1(t) computes block 0 of S^T of tile t+1 on the matrix
+// core beside the exponentials of tile t, then O^T += block 0 of tile t;
+// h2(t) computes block 1 of S^T(t+1), O^T += block 1 of tile t and the column
+// max of tile t+1.  Waves w and
 // w + 4 share a SIMD: waves 0-3 run h1(t) h2(t) after barrier t, waves 4-7 run
 // h2(t-1) h1(t), half an iteration later, so on every SIMD one wave's
 // exponentials run beside the other's matrix work instead of both waves
@@ -41,9 +43,11 @@
 // conflicts on the 64-bank LDS.
 // Workgroups are renumbered so that consecutive Q tiles of one head land on
 // the same XCD (the hardware deals workgroups to the 8 XCDs round robin) and
-// share that XCD's L2 for the head's K/V.  When the units do not fill the last
-// round of the GPU, the host splits that round's units along their keys into
-// up to four parts (unnormalised fp32 partials, merged by tail_merge_kernel).
+// share that XCD's L2 for the head's K/V (a packed clip deals whole (chunk,
+// head) groups round robin instead, since its chunks' read sets differ in
+// length).  When the units do not fill the last round of the GPU, the host
+// splits that round's units along their keys into up to four parts
+// (unnormalised fp32 partials, merged by tail_merge_kernel).
 
 #include <hip/hip_runtime.h>
 
