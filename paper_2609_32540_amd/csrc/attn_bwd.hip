@@ -434,24 +434,27 @@ __device__ inline int xcd_interleaved(int b, int n_wg, int group) {
 }
 
 // ---- D_i = dO_i . O_i ---------------------------------------------------------------
+// L = d / 8 consecutive lanes per row (16 bytes of O and of dO each, so a wave
+// reads contiguous memory), partial sums combined across the L lanes.
+template <int L>
 __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict__ o,
                                                         const __bf16* __restrict__ dout,
-                                                        float* __restrict__ delta, int64_t rows,
-                                                        int d) {
-  const int64_t r = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (r >= rows) return;
-  const u32x4* po = reinterpret_cast<const u32x4*>(o + r * d);
-  const u32x4* pd = reinterpret_cast<const u32x4*>(dout + r * d);
+                                                        float* __restrict__ delta, int64_t rows) {
+  const int64_t t = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t r = t / L;
   float acc = 0.0f;
-  for (int c = 0; c < d / 8; ++c) {
-    const u32x4 a = po[c], b = pd[c];
+  if (r < rows) {
+    const u32x4 a = reinterpret_cast<const u32x4*>(o)[t];
+    const u32x4 b = reinterpret_cast<const u32x4*>(dout)[t];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       acc = fmaf(__uint_as_float(a[j] << 16), __uint_as_float(b[j] << 16), acc);
       acc = fmaf(__uint_as_float(a[j] & 0xffff0000u), __uint_as_float(b[j] & 0xffff0000u), acc);
     }
   }
-  delta[r] = acc;
+#pragma unroll
+  for (int off = L / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, L);
+  if (r < rows && (t % L) == 0) delta[r] = acc;
 }
 
 // ---- dQ: query-stationary ---------------------------------------------------------------
@@ -740,9 +743,16 @@ hipError_t launch_attention_bwd_bf16(const void* q, const void* out, const void*
   const int nq = plan.chunk_tokens;
   const int64_t rows = int64_t(plan.n_chunks) * nq * heads;
   if (rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(bwd_delta_kernel, dim3(unsigned((rows + 255) / 256)), dim3(256), 0, stream,
-                     static_cast<const __bf16*>(out), static_cast<const __bf16*>(dout), delta, rows,
-                     head_dim);
+  {
+    const int64_t threads = rows * (head_dim / 8);   // the last block may run past the rows
+    const dim3 g(unsigned((threads + 255) / 256));
+    if (head_dim == 128)
+      hipLaunchKernelGGL(bwd_delta_kernel<16>, g, dim3(256), 0, stream,
+                         static_cast<const __bf16*>(out), static_cast<const __bf16*>(dout), delta, rows);
+    else
+      hipLaunchKernelGGL(bwd_delta_kernel<8>, g, dim3(256), 0, stream,
+                         static_cast<const __bf16*>(out), static_cast<const __bf16*>(dout), delta, rows);
+  }
   const float c_log2 = float(double(softmax_scale) * 1.4426950408889634);
   const int n_qtiles = (nq + kBlockN - 1) / kBlockN;
   KeyUnits ku;
