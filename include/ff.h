@@ -283,7 +283,7 @@ size_t ff_packed_attention_bwd_workspace(const ff_packed_desc* desc);
  * `workspace` (device, ff_packed_attention_bwd_workspace() bytes, 16-byte
  * aligned) holds rowsum(dO * O).  At most 64 anchor frames, and the chunks
  * that see one frame may form at most 8 runs of consecutive chunks
- * (FF_ERR_UNSUPPORTED).  Host validation, then four launches. */
+ * (FF_ERR_UNSUPPORTED).  Host validation, then three launches. */
 ff_status ff_packed_attention_bwd(const ff_packed_desc* desc, const void* q, const void* k,
                                   const void* v, const void* anchor_k, const void* anchor_v,
                                   const void* out, const void* dout, const float* lse, void* dq,

@@ -18,6 +18,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <new>
 #include <string>
 #include <vector>
@@ -29,19 +30,33 @@ namespace {
 
 thread_local std::string g_last_error;
 
-ff_status fail(ff_status st, const char* fmt, ...) {
+// No exception crosses the C ABI: the message is best effort, and entry points
+// that allocate host bookkeeping run their body under no_throw().
+ff_status fail(ff_status st, const char* fmt, ...) noexcept {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
   vsnprintf(buf, sizeof(buf), fmt, ap);
   va_end(ap);
-  g_last_error = buf;
+  try {
+    g_last_error = buf;
+  } catch (...) {
+  }
   return st;
 }
 
-ff_status ok() {
+ff_status ok() noexcept {
   g_last_error.clear();
   return FF_OK;
+}
+
+template <class F>
+ff_status no_throw(F&& body) noexcept {
+  try {
+    return body();
+  } catch (...) {
+    return fail(FF_ERR_INVALID_ARG, "out of host memory");
+  }
 }
 
 constexpr size_t kAlign = 256;
@@ -220,27 +235,29 @@ size_t ff_cache_bytes(const ff_cache_desc* desc) {
 
 ff_status ff_cache_create(const ff_cache_desc* desc, void* dev_buf, size_t dev_bytes,
                           ff_cache** out) {
-  if (!out) return fail(FF_ERR_INVALID_ARG, "out is NULL");
-  ff_status st = check_desc(desc);
-  if (st != FF_OK) return st;
-  if (!dev_buf) return fail(FF_ERR_INVALID_ARG, "dev_buf is NULL");
-  if (reinterpret_cast<uintptr_t>(dev_buf) % kAlign != 0)
-    return fail(FF_ERR_BUFFER, "dev_buf must be %zu-byte aligned", kAlign);
-  const Layout L = make_layout(desc);
-  if (dev_bytes < L.total)
-    return fail(FF_ERR_BUFFER, "dev_bytes %zu < required %zu", dev_bytes, L.total);
-  ff_cache* c = new (std::nothrow) ff_cache;
-  if (!c) return fail(FF_ERR_INVALID_ARG, "out of host memory");
-  c->desc = *desc;
-  c->layout = L;
-  c->dev = static_cast<char*>(dev_buf);
-  const size_t rings = size_t(desc->num_stages) * desc->num_layers;
-  c->slot_chunk.assign(rings * desc->ring_chunks, -1);
-  c->next_chunk.assign(rings, -1);
-  c->anchor_frames.assign(size_t(desc->num_layers) * (desc->max_anchor_frames + 1), 0);
-  c->anchor_count.assign(desc->num_layers, 0);
-  *out = c;
-  return ok();
+  return no_throw([&]() -> ff_status {
+    if (!out) return fail(FF_ERR_INVALID_ARG, "out is NULL");
+    ff_status st = check_desc(desc);
+    if (st != FF_OK) return st;
+    if (!dev_buf) return fail(FF_ERR_INVALID_ARG, "dev_buf is NULL");
+    if (reinterpret_cast<uintptr_t>(dev_buf) % kAlign != 0)
+      return fail(FF_ERR_BUFFER, "dev_buf must be %zu-byte aligned", kAlign);
+    const Layout L = make_layout(desc);
+    if (dev_bytes < L.total)
+      return fail(FF_ERR_BUFFER, "dev_bytes %zu < required %zu", dev_bytes, L.total);
+    std::unique_ptr<ff_cache> c(new (std::nothrow) ff_cache);
+    if (!c) return fail(FF_ERR_INVALID_ARG, "out of host memory");
+    c->desc = *desc;
+    c->layout = L;
+    c->dev = static_cast<char*>(dev_buf);
+    const size_t rings = size_t(desc->num_stages) * desc->num_layers;
+    c->slot_chunk.assign(rings * desc->ring_chunks, -1);
+    c->next_chunk.assign(rings, -1);
+    c->anchor_frames.assign(size_t(desc->num_layers) * (desc->max_anchor_frames + 1), 0);
+    c->anchor_count.assign(desc->num_layers, 0);
+    *out = c.release();
+    return ok();
+  });
 }
 
 ff_status ff_cache_destroy(ff_cache* cache) {
@@ -439,8 +456,10 @@ ff_status chunk_attention_impl(ff_cache* cache, int32_t stage, int32_t layer, in
 ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
                              const void* q, const void* k_cur, const void* v_cur, void* out,
                              float softmax_scale, void* stream) {
-  return chunk_attention_impl(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
-                              softmax_scale, nullptr, nullptr, 0, nullptr, stream);
+  return no_throw([&]() -> ff_status {
+    return chunk_attention_impl(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
+                                softmax_scale, nullptr, nullptr, 0, nullptr, stream);
+  });
 }
 
 ff_status ff_chunk_attention_bank(ff_cache* cache, int32_t stage, int32_t layer,
@@ -448,9 +467,11 @@ ff_status ff_chunk_attention_bank(ff_cache* cache, int32_t stage, int32_t layer,
                                   const void* v_cur, void* out, float softmax_scale,
                                   const void* bank_k, const void* bank_v, int32_t n_frames,
                                   const int32_t* frame_index, void* stream) {
-  if (!bank_k) return fail(FF_ERR_INVALID_ARG, "bank_k must be non-NULL");
-  return chunk_attention_impl(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
-                              softmax_scale, bank_k, bank_v, n_frames, frame_index, stream);
+  return no_throw([&]() -> ff_status {
+    if (!bank_k) return fail(FF_ERR_INVALID_ARG, "bank_k must be non-NULL");
+    return chunk_attention_impl(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
+                                softmax_scale, bank_k, bank_v, n_frames, frame_index, stream);
+  });
 }
 
 ff_status ff_cache_ring_state(const ff_cache* cache, int32_t stage, int32_t layer,
@@ -623,60 +644,62 @@ ff_status ff_packed_attention_bwd(const ff_packed_desc* desc, const void* q, con
                                   void* dk, void* dv, void* d_anchor_k, void* d_anchor_v,
                                   float softmax_scale, void* workspace, size_t workspace_bytes,
                                   void* stream) {
-  ff::PackedPlan plan;
-  ff_status st = make_packed_plan(desc, q, k, v, anchor_k, anchor_v, out, softmax_scale, &plan);
-  if (st != FF_OK) return st;
-  const ff_packed_desc& d = *desc;
-  if (d.dtype != FF_DT_BF16) return fail(FF_ERR_UNSUPPORTED, "the backward pass is bf16 only");
-  if (d.n_anchor_frames > 64)
-    return fail(FF_ERR_UNSUPPORTED, "the backward pass takes at most 64 anchor frames");
-  if (!dout || !lse || !dq || !dk || !dv || !workspace)
-    return fail(FF_ERR_INVALID_ARG, "dout, lse, dq, dk, dv and workspace must be non-NULL");
-  if (d.n_anchor_frames > 0 && (!d_anchor_k || !d_anchor_v))
-    return fail(FF_ERR_INVALID_ARG, "d_anchor_k / d_anchor_v must be non-NULL with anchor frames");
-  if (check_aligned(dout, "dout") != FF_OK || check_aligned(dq, "dq") != FF_OK ||
-      check_aligned(dk, "dk") != FF_OK || check_aligned(dv, "dv") != FF_OK ||
-      check_aligned(workspace, "workspace") != FF_OK ||
-      (d.n_anchor_frames > 0 && (check_aligned(d_anchor_k, "d_anchor_k") != FF_OK ||
-                                 check_aligned(d_anchor_v, "d_anchor_v") != FF_OK)))
-    return FF_ERR_INVALID_ARG;
-  if (reinterpret_cast<uintptr_t>(lse) % 4 != 0) return fail(FF_ERR_INVALID_ARG, "lse misaligned");
-  const size_t need = ff_packed_attention_bwd_workspace(desc);
-  if (workspace_bytes < need)
-    return fail(FF_ERR_BUFFER, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
-  // chunks that see each anchor frame, as runs of consecutive chunks
-  std::vector<std::array<uint8_t, 16>> frame_runs(std::max(d.n_anchor_frames, 1));
-  for (int f = 0; f < d.n_anchor_frames; ++f) {
-    std::fill(frame_runs[f].begin(), frame_runs[f].end(), uint8_t(0));
-    int n = 0;
-    for (int c = 0; c < d.n_chunks;) {
-      bool sees = false;
-      for (int j = 0; j < FF_MAX_ANCHOR_FRAMES; ++j)
-        sees |= d.anchors_of_chunk[c * FF_MAX_ANCHOR_FRAMES + j] == f;
-      if (!sees) { ++c; continue; }
-      int e = c + 1;
-      for (; e < d.n_chunks; ++e) {
-        bool s2 = false;
+  return no_throw([&]() -> ff_status {
+    ff::PackedPlan plan;
+    ff_status st = make_packed_plan(desc, q, k, v, anchor_k, anchor_v, out, softmax_scale, &plan);
+    if (st != FF_OK) return st;
+    const ff_packed_desc& d = *desc;
+    if (d.dtype != FF_DT_BF16) return fail(FF_ERR_UNSUPPORTED, "the backward pass is bf16 only");
+    if (d.n_anchor_frames > 64)
+      return fail(FF_ERR_UNSUPPORTED, "the backward pass takes at most 64 anchor frames");
+    if (!dout || !lse || !dq || !dk || !dv || !workspace)
+      return fail(FF_ERR_INVALID_ARG, "dout, lse, dq, dk, dv and workspace must be non-NULL");
+    if (d.n_anchor_frames > 0 && (!d_anchor_k || !d_anchor_v))
+      return fail(FF_ERR_INVALID_ARG, "d_anchor_k / d_anchor_v must be non-NULL with anchor frames");
+    if (check_aligned(dout, "dout") != FF_OK || check_aligned(dq, "dq") != FF_OK ||
+        check_aligned(dk, "dk") != FF_OK || check_aligned(dv, "dv") != FF_OK ||
+        check_aligned(workspace, "workspace") != FF_OK ||
+        (d.n_anchor_frames > 0 && (check_aligned(d_anchor_k, "d_anchor_k") != FF_OK ||
+                                   check_aligned(d_anchor_v, "d_anchor_v") != FF_OK)))
+      return FF_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(lse) % 4 != 0) return fail(FF_ERR_INVALID_ARG, "lse misaligned");
+    const size_t need = ff_packed_attention_bwd_workspace(desc);
+    if (workspace_bytes < need)
+      return fail(FF_ERR_BUFFER, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    // chunks that see each anchor frame, as runs of consecutive chunks
+    std::vector<std::array<uint8_t, 16>> frame_runs(std::max(d.n_anchor_frames, 1));
+    for (int f = 0; f < d.n_anchor_frames; ++f) {
+      std::fill(frame_runs[f].begin(), frame_runs[f].end(), uint8_t(0));
+      int n = 0;
+      for (int c = 0; c < d.n_chunks;) {
+        bool sees = false;
         for (int j = 0; j < FF_MAX_ANCHOR_FRAMES; ++j)
-          s2 |= d.anchors_of_chunk[e * FF_MAX_ANCHOR_FRAMES + j] == f;
-        if (!s2) break;
+          sees |= d.anchors_of_chunk[c * FF_MAX_ANCHOR_FRAMES + j] == f;
+        if (!sees) { ++c; continue; }
+        int e = c + 1;
+        for (; e < d.n_chunks; ++e) {
+          bool s2 = false;
+          for (int j = 0; j < FF_MAX_ANCHOR_FRAMES; ++j)
+            s2 |= d.anchors_of_chunk[e * FF_MAX_ANCHOR_FRAMES + j] == f;
+          if (!s2) break;
+        }
+        if (n == 8)
+          return fail(FF_ERR_UNSUPPORTED, "anchor frame %d is seen by more than 8 runs of chunks", f);
+        if (int64_t(e - c) * d.chunk_tokens * 2 * d.num_heads * d.head_dim > int64_t(UINT32_MAX))
+          return fail(FF_ERR_UNSUPPORTED, "a run of chunks spans more than 4 GiB");
+        frame_runs[f][2 * n] = uint8_t(c);
+        frame_runs[f][2 * n + 1] = uint8_t(e - c);
+        ++n;
+        c = e;
       }
-      if (n == 8)
-        return fail(FF_ERR_UNSUPPORTED, "anchor frame %d is seen by more than 8 runs of chunks", f);
-      if (int64_t(e - c) * d.chunk_tokens * 2 * d.num_heads * d.head_dim > int64_t(UINT32_MAX))
-        return fail(FF_ERR_UNSUPPORTED, "a run of chunks spans more than 4 GiB");
-      frame_runs[f][2 * n] = uint8_t(c);
-      frame_runs[f][2 * n + 1] = uint8_t(e - c);
-      ++n;
-      c = e;
     }
-  }
-  hipError_t e = ff::launch_attention_bwd_bf16(
-      q, out, dout, lse, static_cast<float*>(workspace), dq, dk, dv, d_anchor_k, d_anchor_v,
-      d.num_heads, d.head_dim, softmax_scale, plan,
-      reinterpret_cast<const uint8_t(*)[16]>(frame_runs.data()), d.n_anchor_frames,
-      static_cast<hipStream_t>(stream));
-  return hip_status(e, "packed_attention_bwd launch");
+    hipError_t e = ff::launch_attention_bwd_bf16(
+        q, out, dout, lse, static_cast<float*>(workspace), dq, dk, dv, d_anchor_k, d_anchor_v,
+        d.num_heads, d.head_dim, softmax_scale, plan,
+        reinterpret_cast<const uint8_t(*)[16]>(frame_runs.data()), d.n_anchor_frames,
+        static_cast<hipStream_t>(stream));
+    return hip_status(e, "packed_attention_bwd launch");
+  });
 }
 
 ff_status ff_anchor_partition(int32_t L, int32_t delta, int32_t* out, int32_t capacity,
@@ -733,44 +756,53 @@ ff_status ff_euler_step(const void* x, const void* v, void* x_out, int64_t n, do
 ff_status ff_wavefront_run(int64_t n_chunks, int32_t n_stages, void* const* streams,
                            ff_stage_forward_fn forward, void* user, int64_t* n_rounds,
                            int64_t* n_forwards) {
-  if (n_chunks < 1 || n_stages < 1 || n_stages > 64)
-    return fail(FF_ERR_INVALID_ARG, "need n_chunks >= 1 and 1 <= n_stages <= 64");
-  if (!streams || !forward) return fail(FF_ERR_INVALID_ARG, "streams and forward must be non-NULL");
-  std::vector<hipEvent_t> done(n_stages, nullptr);   // done[s]: rank s's latest forward
-  ff_status st = FF_OK;
-  for (int s = 0; s < n_stages && st == FF_OK; ++s)
-    if (hipEventCreateWithFlags(&done[s], hipEventDisableTiming) != hipSuccess)
-      st = fail(FF_ERR_HIP, "hipEventCreateWithFlags failed");
-  const int64_t rounds = n_chunks + n_stages - 1;
-  int64_t forwards = 0;
-  for (int64_t n = 0; n < rounds && st == FF_OK; ++n) {
-    // ranks in descending order: rank s waits on rank s-1's forward of the same
-    // chunk (round n-1) before rank s-1 records its next one in this round
-    for (int s = n_stages - 1; s >= 0 && st == FF_OK; --s) {
-      const int64_t i = n - s;
-      if (i < 0 || i >= n_chunks) continue;
-      hipStream_t hs = static_cast<hipStream_t>(streams[s]);
-      if (s > 0 && hipStreamWaitEvent(hs, done[s - 1], 0) != hipSuccess) {
-        st = fail(FF_ERR_HIP, "hipStreamWaitEvent failed");
-        break;
+  return no_throw([&]() -> ff_status {
+    if (n_chunks < 1 || n_stages < 1 || n_stages > 64)
+      return fail(FF_ERR_INVALID_ARG, "need n_chunks >= 1 and 1 <= n_stages <= 64");
+    if (!streams || !forward) return fail(FF_ERR_INVALID_ARG, "streams and forward must be non-NULL");
+    // done[s]: rank s's latest forward (destroyed on every way out)
+    struct Events {
+      std::vector<hipEvent_t> e;
+      ~Events() {
+        for (hipEvent_t x : e)
+          if (x) (void)hipEventDestroy(x);
       }
-      const int32_t r = forward(user, s, i, streams[s]);
-      if (r != FF_OK) {
-        st = (r >= 1 && r <= 7) ? ff_status(r) : FF_ERR_INVALID_ARG;
-        if (g_last_error.empty())
-          fail(st, "forward of stage %d, chunk %lld returned %d", s, (long long)i, r);
-        break;
+    } ev;
+    ev.e.assign(n_stages, nullptr);
+    std::vector<hipEvent_t>& done = ev.e;
+    ff_status st = FF_OK;
+    for (int s = 0; s < n_stages && st == FF_OK; ++s)
+      if (hipEventCreateWithFlags(&done[s], hipEventDisableTiming) != hipSuccess)
+        st = fail(FF_ERR_HIP, "hipEventCreateWithFlags failed");
+    const int64_t rounds = n_chunks + n_stages - 1;
+    int64_t forwards = 0;
+    for (int64_t n = 0; n < rounds && st == FF_OK; ++n) {
+      // ranks in descending order: rank s waits on rank s-1's forward of the same
+      // chunk (round n-1) before rank s-1 records its next one in this round
+      for (int s = n_stages - 1; s >= 0 && st == FF_OK; --s) {
+        const int64_t i = n - s;
+        if (i < 0 || i >= n_chunks) continue;
+        hipStream_t hs = static_cast<hipStream_t>(streams[s]);
+        if (s > 0 && hipStreamWaitEvent(hs, done[s - 1], 0) != hipSuccess) {
+          st = fail(FF_ERR_HIP, "hipStreamWaitEvent failed");
+          break;
+        }
+        const int32_t r = forward(user, s, i, streams[s]);
+        if (r != FF_OK) {
+          st = (r >= 1 && r <= 7) ? ff_status(r) : FF_ERR_INVALID_ARG;
+          if (g_last_error.empty())
+            fail(st, "forward of stage %d, chunk %lld returned %d", s, (long long)i, r);
+          break;
+        }
+        ++forwards;
+        if (hipEventRecord(done[s], hs) != hipSuccess) st = fail(FF_ERR_HIP, "hipEventRecord failed");
       }
-      ++forwards;
-      if (hipEventRecord(done[s], hs) != hipSuccess) st = fail(FF_ERR_HIP, "hipEventRecord failed");
     }
-  }
-  for (hipEvent_t e : done)
-    if (e) (void)hipEventDestroy(e);
-  if (st != FF_OK) return st;
-  if (n_rounds) *n_rounds = rounds;
-  if (n_forwards) *n_forwards = forwards;
-  return ok();
+    if (st != FF_OK) return st;
+    if (n_rounds) *n_rounds = rounds;
+    if (n_forwards) *n_forwards = forwards;
+    return ok();
+  });
 }
 
 const char* ff_status_string(ff_status status) {
