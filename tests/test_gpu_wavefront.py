@@ -73,11 +73,14 @@ def make_stub(cache, w, X, layers, bank=None):
     return forward
 
 
-@pytest.mark.parametrize("N_R,layers", [(6, 2), (3, 1)])
-def test_wavefront_equals_chunk_major(N_R, layers):
+# W = 4 gives read sets of up to 23 key tiles: the attention's tail split runs (two key
+# parts per unit) with each stage's partials in its own scratch while the stages run
+# concurrently
+@pytest.mark.parametrize("N_R,layers,W", [(6, 2, 2), (3, 1, 2), (7, 1, 4)])
+def test_wavefront_equals_chunk_major(N_R, layers, W):
     S = len(SIGMAS) - 1
     w = synth.small_workload("wave", dtype="bf16", heads=2, head_dim=128, grid_h=6, grid_w=11,
-                             ring_chunks=2, stages=S, layers=layers, n_chunks=N_R,
+                             ring_chunks=W, stages=S, layers=layers, n_chunks=N_R,
                              anchor_rule="fixed:0,7", max_anchor_frames=2)
     dev = torch.device("cuda", 0)
     g = torch.Generator(device=dev)
