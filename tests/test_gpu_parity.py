@@ -252,6 +252,31 @@ def test_attention_maximum_segments(dtype, head_dim, grid):
     assert count == w.n_chunks and sorted(table) == list(range(w.n_chunks - W, w.n_chunks))
 
 
+@pytest.mark.parametrize("head_dim,heads,grid", [(128, 3, (6, 11)), (64, 2, (12, 22))])
+def test_attention_running_max_rescales(head_dim, heads, grid):
+    # Keys of later chunks scaled by 1, 3, 9, 27, ..: each new segment carries
+    # logits far above the running max (the rescale path runs again and again,
+    # also inside tail-split key parts), then a chunk whose own keys are tiny
+    # (no rescale, probabilities underflow to 0 for most keys).
+    W = 4
+    w = small("bf16", head_dim, heads=heads, grid_h=grid[0], grid_w=grid[1], ring_chunks=W,
+              stages=1, layers=1, n_chunks=7, anchor_rule="none", max_anchor_frames=1)
+    cache = make_cache(w, 1, 1)
+    hist = []
+    for c in range(w.n_chunks):
+        q, k, v = (synth.chunk_tensor(w, t, c, 0, 0) for t in (synth.T_Q, synth.T_K, synth.T_V))
+        factor = 3.0 ** c if c < w.n_chunks - 1 else 1.0 / 64
+        k = (k.float() * factor).to(torch.bfloat16)
+        out = cache.chunk_attention(0, 0, c, to_dev(q), to_dev(k), to_dev(v))
+        cache.kv_publish(0, 0, c, to_dev(k), to_dev(v))
+        K_all = np.concatenate([h[0] for h in hist] + [exact(k)])
+        V_all = np.concatenate([h[1] for h in hist] + [exact(v)])
+        ref = fo.masked_attention(exact(q), K_all, V_all, np.ones(len(K_all), bool),
+                                  1.0 / math.sqrt(head_dim))
+        check_attention(exact(out), ref, "bf16", f"chunk {c} (key scale {factor:g})")
+        hist = (hist + [(exact(k), exact(v))])[-W:]
+
+
 def test_unfilled_slots_poisoned_with_nan_are_never_read():
     w = small("bf16", 128, ring_chunks=4, anchor_rule="fixed:3", max_anchor_frames=3)
     run = PairedRun(w, poison=True)
