@@ -40,15 +40,15 @@ def check_grad(got, ref, what):
     return rl
 
 
-def run_case(n, Nq, G, n_frames, table, W, heads, d, seed=0, hidden_frame=False):
+def run_case(n, Nq, G, n_frames, table, W, heads, d, seed=0, hidden_frame=False, key_scale=1.0):
     dev = torch.device("cuda", 0)
     g = torch.Generator(device=dev)
     g.manual_seed(seed)
 
     def rnd(shape, s=1.0):
         return (torch.randn(shape, generator=g, device=dev) * s).to(torch.bfloat16)
-    q, k, v = rnd((n * Nq, heads, d)), rnd((n * Nq, heads, d)), rnd((n * Nq, heads, d))
-    ak, av = rnd((n_frames * G, heads, d)), rnd((n_frames * G, heads, d))
+    q, k, v = rnd((n * Nq, heads, d)), rnd((n * Nq, heads, d), key_scale), rnd((n * Nq, heads, d))
+    ak, av = rnd((n_frames * G, heads, d), key_scale), rnd((n_frames * G, heads, d))
     dout = rnd((n * Nq, heads, d))
     scale = 1.0 / math.sqrt(d)
     lse = torch.empty((n * Nq, heads), dtype=torch.float32, device=dev)
@@ -93,6 +93,13 @@ def test_backward_one_and_two_tile_streams(d, W):
     # 20-token chunks and 10-token frames: every workgroup streams one to
     # three partial tiles, so the ring schedules run their shortest loops
     run_case(3, 20, 10, 2, [[0], [], [0, 1]], W, 3, d, seed=11)
+
+
+@pytest.mark.parametrize("d", [128, 64])
+def test_backward_peaked_softmax(d):
+    # keys scaled by 6: logits of several standard deviations, P close to one-hot
+    # for many rows; P is rebuilt from the forward's log-sum-exp
+    run_case(6, 198, 66, 3, TABLE6, 2, 2, d, seed=13, key_scale=6.0)
 
 
 def test_backward_multi_tile_and_hidden_frame():
