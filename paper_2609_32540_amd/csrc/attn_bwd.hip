@@ -50,7 +50,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBlockN = 32 * kWaves;   // stationary columns (queries or keys) per workgroup
-constexpr int kBT = 64;                // streamed rows per tile (32 for the d = 128 dK pass)
+constexpr int kBT = 64;                // streamed rows per tile (32 in the d = 128 dK/dV pass)
 constexpr int kXcds = 8;
 constexpr int kMaxRuns = 2 * FF_MAX_ANCHOR_FRAMES + 1;   // segments of one streamed set
 
