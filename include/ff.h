@@ -60,9 +60,10 @@
 extern "C" {
 #endif
 
-#define FF_ABI_VERSION 2
+#define FF_ABI_VERSION 3
 #define FF_MAX_RING_CHUNKS 8     /* W <= 8 */
 #define FF_MAX_ANCHOR_FRAMES 8   /* anchor frames per layer */
+#define FF_MAX_BATCH 4           /* items per ff_chunk_attention_batch call */
 #define FF_MAX_ROPE_FRAMES 16    /* frames per ff_rope3d call */
 #define FF_MAX_PACKED_CHUNKS 128 /* chunks per ff_packed_attention call */
 
@@ -200,6 +201,35 @@ ff_status ff_chunk_attention_bank(ff_cache* cache, int32_t stage, int32_t layer,
                                   const void* v_cur, void* out, float softmax_scale,
                                   const void* bank_k, const void* bank_v, int32_t n_frames,
                                   const int32_t* frame_index, void* stream);
+
+/* One item of ff_chunk_attention_batch: the arguments of one
+ * ff_chunk_attention call (bank_k == NULL) or ff_chunk_attention_bank call. */
+typedef struct {
+  int32_t stage;
+  int32_t layer;
+  int64_t chunk_index;
+  const void* q;
+  const void* k_cur;
+  const void* v_cur;
+  void* out;
+  const void* bank_k;          /* NULL: the layer's anchor segment */
+  const void* bank_v;
+  int32_t n_frames;
+  int32_t reserved;
+  const int32_t* frame_index;  /* host, n_frames entries */
+} ff_attention_item;
+
+/* The attention of 1 <= n <= FF_MAX_BATCH independent items in one launch,
+ * e.g. the stages' forwards of one wavefront round (chunk i at stage s, chunk
+ * i-1 at stage s+1, ..), which on one GPU fill it better together than one
+ * after another.  Item j computes exactly what its ff_chunk_attention(_bank)
+ * call would, bit for bit: the batch is never split along keys (Sec. 3.1 and
+ * App. Alg. 1, the Evaluate step of every rank of a round).  Items share
+ * softmax_scale; each is validated as its single call would be, all before
+ * anything is enqueued.  Items may read the same ring; their outputs must not
+ * overlap each other or any input. */
+ff_status ff_chunk_attention_batch(ff_cache* cache, int32_t n, const ff_attention_item* items,
+                                   float softmax_scale, void* stream);
 
 /* Host bookkeeping of one ring: slot_chunk[s] (W entries, host) is the chunk
  * held by slot s or -1; *published_count is the next chunk the ring expects

@@ -147,6 +147,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, int nq, int heads,
                       float scale_log2, Src src, int n_qtiles, TailSplit tail) {
   constexpr bool kPacked = __is_same(Src, PackedPlan);
+  constexpr bool kBatch = __is_same(Src, KvBatch);
+  constexpr bool kSets = kPacked || kBatch;   // one read set per (chunk or item) of the grid
   using C = Cfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
   __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
@@ -159,13 +161,13 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   // unit n_full + (b - n_full) / split (the partial last round, see TailSplit).
   const int b = blockIdx.x;
   int logical, part_id = 0, n_parts = 1;
-  const int n_pairs = kPacked ? gridDim.x / n_qtiles : 0;      // (chunk, head) pairs
+  const int n_pairs = kSets ? gridDim.x / n_qtiles : 0;       // (set, head) pairs
   const int n_even = n_pairs - n_pairs % kXcds;
-  if (kPacked) {
-    // packed clip: the chunks' read sets differ in length, so XCD x takes the
-    // (chunk, head) pairs p = x, x + 8, .. (the q tiles of one pair stay on one
-    // XCD and share its L2): every XCD gets the same mix of chunks; the last
-    // n_pairs % 8 pairs run in order
+  if (kSets) {
+    // several read sets (packed chunks, batch items) of different lengths: XCD
+    // x takes the (set, head) pairs p = x, x + 8, .. (the q tiles of one pair
+    // stay on one XCD and share its L2), so every XCD gets the same mix; the
+    // last n_pairs % 8 pairs run in order
     if (b < n_even * n_qtiles) {
       const int xcd = b % kXcds, idx = b / kXcds;
       logical = (xcd + kXcds * (idx / n_qtiles)) * n_qtiles + idx % n_qtiles;
@@ -183,12 +185,18 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     part_id = j % tail.split;
     n_parts = tail.split;
   }
-  int chunk = 0, rest = logical;
-  if constexpr (kPacked) {
+  int chunk = 0, rest = logical;   // chunk: the read set (packed chunk or batch item)
+  if constexpr (kSets) {
     chunk = logical / (heads * n_qtiles);
     rest = logical - chunk * (heads * n_qtiles);
+  }
+  if constexpr (kPacked) {
     q += int64_t(chunk) * nq * heads * D;
     out += int64_t(chunk) * nq * heads * D;
+  }
+  if constexpr (kBatch) {
+    q = static_cast<const __bf16*>(src.q[chunk]);
+    out = static_cast<__bf16*>(src.out[chunk]);
   }
   const int head = rest / n_qtiles;
   const int qt = rest % n_qtiles;
@@ -234,12 +242,14 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   uint64_t sg_k = 0, sg_v = 0;
   int n_segs;
   if constexpr (kPacked) n_segs = packed_num_segments(src, chunk);
+  else if constexpr (kBatch) n_segs = src.set[chunk].n;
   else n_segs = src.n;
 #pragma unroll
   for (int i = 0; i < kMaxSegments; ++i)
     if (lane == i && i < n_segs) {
       KvSegment sgi;
       if constexpr (kPacked) sgi = packed_segment(src, chunk, i, heads, D, 2);
+      else if constexpr (kBatch) sgi = src.set[chunk].seg[i];
       else sgi = src.seg[i];
       sg_len = sgi.len;
       sg_row_bytes = 2u * uint32_t(sgi.tok_stride);
@@ -637,6 +647,22 @@ hipError_t launch_attention_bf16(const void* q, void* out, int nq, int heads, in
       hipLaunchKernelGGL(tail_merge_kernel<64>, g, dim3(256), 0, stream, tail.part,
                          static_cast<__bf16*>(out), nq, heads, n_qtiles, tail, n_tail);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_bf16_batch(int nq, int heads, int head_dim, float softmax_scale,
+                                       const KvBatch& b, hipStream_t stream) {
+  if (nq <= 0 || b.n <= 0) return hipSuccess;
+  const int n_qtiles = (nq + kBlockQ - 1) / kBlockQ;
+  const dim3 grid(b.n * n_qtiles * heads);
+  const float scale_log2 = float(double(softmax_scale) * 1.4426950408889634);
+  const TailSplit whole = {int(grid.x), 1, nullptr};
+  if (head_dim == 128)
+    hipLaunchKernelGGL((attn_bf16_kernel<128, KvBatch>), grid, dim3(kThreads), 0, stream,
+                       nullptr, nullptr, nq, heads, scale_log2, b, n_qtiles, whole);
+  else
+    hipLaunchKernelGGL((attn_bf16_kernel<64, KvBatch>), grid, dim3(kThreads), 0, stream,
+                       nullptr, nullptr, nq, heads, scale_log2, b, n_qtiles, whole);
   return hipGetLastError();
 }
 

@@ -2,9 +2,9 @@
 // tiles staged in LDS, online softmax in float32 with expf.  Small sizes
 // only; the bf16 kernel is the fast path.
 //
-// Launch shape: grid (ceil(nq / 128), heads, chunks), 128 threads; the read
-// set is one KvSegments for the launch or, for a packed clip, the PackedPlan
-// segments of chunk blockIdx.z.
+// Launch shape: grid (ceil(nq / 128), heads, sets), 128 threads; the read
+// set is one KvSegments for the launch, for a packed clip the PackedPlan
+// segments of chunk blockIdx.z, for a batch the set of item blockIdx.z.
 
 #include <hip/hip_runtime.h>
 
@@ -23,9 +23,15 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(const float* __restr
                                                             float* __restrict__ out, int nq,
                                                             int heads, float scale, Src src) {
   constexpr bool kPacked = __is_same(Src, PackedPlan);
+  constexpr bool kBatch = __is_same(Src, KvBatch);
   const int chunk = blockIdx.z;
-  q += int64_t(chunk) * nq * heads * D;
-  out += int64_t(chunk) * nq * heads * D;
+  if constexpr (kBatch) {
+    q = static_cast<const float*>(src.q[chunk]);
+    out = static_cast<float*>(src.out[chunk]);
+  } else {
+    q += int64_t(chunk) * nq * heads * D;
+    out += int64_t(chunk) * nq * heads * D;
+  }
   __shared__ float ks[kTileK][D];
   __shared__ float vs[kTileK][D];
   const int head = blockIdx.y;
@@ -43,10 +49,12 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(const float* __restr
 
   int n_segs;
   if constexpr (kPacked) n_segs = packed_num_segments(src, chunk);
+  else if constexpr (kBatch) n_segs = src.set[chunk].n;
   else n_segs = src.n;
   for (int sg = 0; sg < n_segs; ++sg) {
     KvSegment seg;
     if constexpr (kPacked) seg = packed_segment(src, chunk, sg, heads, D, 4);
+    else if constexpr (kBatch) seg = src.set[chunk].seg[sg];
     else seg = src.seg[sg];
     const float* kb = static_cast<const float*>(seg.k) + head * seg.head_stride;
     const float* vb = static_cast<const float*>(seg.v) + head * seg.head_stride;
@@ -100,6 +108,19 @@ hipError_t launch_attention_f32(const void* q, void* out, int nq, int heads, int
     hipLaunchKernelGGL((attn_f32_kernel<128, KvSegments>), grid, dim3(kThreads), 0, stream,
                        static_cast<const float*>(q), static_cast<float*>(out), nq, heads,
                        softmax_scale, segs);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_f32_batch(int nq, int heads, int head_dim, float softmax_scale,
+                                      const KvBatch& b, hipStream_t stream) {
+  if (nq <= 0 || b.n <= 0) return hipSuccess;
+  dim3 grid((nq + kThreads - 1) / kThreads, heads, b.n);
+  if (head_dim == 64)
+    hipLaunchKernelGGL((attn_f32_kernel<64, KvBatch>), grid, dim3(kThreads), 0, stream, nullptr,
+                       nullptr, nq, heads, softmax_scale, b);
+  else
+    hipLaunchKernelGGL((attn_f32_kernel<128, KvBatch>), grid, dim3(kThreads), 0, stream, nullptr,
+                       nullptr, nq, heads, softmax_scale, b);
   return hipGetLastError();
 }
 

@@ -349,10 +349,12 @@ namespace {
 
 // Shared body of ff_chunk_attention and ff_chunk_attention_bank.  bank_k ==
 // nullptr selects the layer's anchor segment.
-ff_status chunk_attention_impl(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
-                               const void* q, const void* k_cur, const void* v_cur, void* out,
-                               float softmax_scale, const void* bank_k, const void* bank_v,
-                               int32_t n_frames, const int32_t* frame_index, void* stream) {
+// Validation and read-set table of one renderer attention call (everything
+// but the softmax scale and the launch).
+ff_status attention_read_set(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
+                             const void* q, const void* k_cur, const void* v_cur, void* out,
+                             const void* bank_k, const void* bank_v, int32_t n_frames,
+                             const int32_t* frame_index, ff::KvSegments* segs_out) {
   if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
   if (!q || !k_cur || !v_cur || !out)
     return fail(FF_ERR_INVALID_ARG, "q, k_cur, v_cur and out must be non-NULL");
@@ -362,8 +364,6 @@ ff_status chunk_attention_impl(ff_cache* cache, int32_t stage, int32_t layer, in
   ff_status st = check_stage_layer(cache, stage, layer);
   if (st != FF_OK) return st;
   if (chunk_index < 0) return fail(FF_ERR_RANGE, "chunk_index %lld < 0", (long long)chunk_index);
-  if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
-    return fail(FF_ERR_INVALID_ARG, "softmax_scale must be positive and finite");
   const ff_cache_desc& d = cache->desc;
   const int G = d.grid_h * d.grid_w;
   const int heads = d.num_heads;
@@ -400,7 +400,7 @@ ff_status chunk_attention_impl(ff_cache* cache, int32_t stage, int32_t layer, in
   const int W = d.ring_chunks;
   const int chunk_tokens = int(cache->layout.chunk_tokens);
 
-  ff::KvSegments segs;
+  ff::KvSegments& segs = *segs_out;
   std::memset(&segs, 0, sizeof(segs));
   auto add = [&](const void* kp, const void* vp, int64_t head_stride, int tok_stride, int len) {
     ff::KvSegment& s = segs.seg[segs.n++];
@@ -435,7 +435,28 @@ ff_status chunk_attention_impl(ff_cache* cache, int32_t stage, int32_t layer, in
   }
   // the chunk itself: token-major
   add(k_cur, v_cur, D, heads * D, chunk_tokens);
+  return FF_OK;
+}
 
+ff_status check_scale(float softmax_scale) {
+  if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
+    return fail(FF_ERR_INVALID_ARG, "softmax_scale must be positive and finite");
+  return FF_OK;
+}
+
+ff_status chunk_attention_impl(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
+                               const void* q, const void* k_cur, const void* v_cur, void* out,
+                               float softmax_scale, const void* bank_k, const void* bank_v,
+                               int32_t n_frames, const int32_t* frame_index, void* stream) {
+  ff::KvSegments segs;
+  ff_status st = attention_read_set(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
+                                    bank_k, bank_v, n_frames, frame_index, &segs);
+  if (st != FF_OK) return st;
+  st = check_scale(softmax_scale);
+  if (st != FF_OK) return st;
+  const ff_cache_desc& d = cache->desc;
+  const int heads = d.num_heads, D = d.head_dim;
+  const int chunk_tokens = int(cache->layout.chunk_tokens);
   hipError_t e;
   if (d.dtype == FF_DT_BF16) {
     const ff::TailSplit tail =
@@ -471,6 +492,39 @@ ff_status ff_chunk_attention_bank(ff_cache* cache, int32_t stage, int32_t layer,
     if (!bank_k) return fail(FF_ERR_INVALID_ARG, "bank_k must be non-NULL");
     return chunk_attention_impl(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
                                 softmax_scale, bank_k, bank_v, n_frames, frame_index, stream);
+  });
+}
+
+ff_status ff_chunk_attention_batch(ff_cache* cache, int32_t n, const ff_attention_item* items,
+                                   float softmax_scale, void* stream) {
+  return no_throw([&]() -> ff_status {
+    if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
+    if (n < 1 || n > FF_MAX_BATCH)
+      return fail(FF_ERR_UNSUPPORTED, "n = %d items; 1 .. %d per batch", n, FF_MAX_BATCH);
+    if (!items) return fail(FF_ERR_INVALID_ARG, "items is NULL");
+    ff_status st = check_scale(softmax_scale);
+    if (st != FF_OK) return st;
+    ff::KvBatch b;
+    std::memset(&b, 0, sizeof(b));
+    for (int j = 0; j < n; ++j) {
+      const ff_attention_item& it = items[j];
+      st = attention_read_set(cache, it.stage, it.layer, it.chunk_index, it.q, it.k_cur, it.v_cur,
+                              it.out, it.bank_k, it.bank_v, it.n_frames, it.frame_index,
+                              &b.set[j]);
+      if (st != FF_OK) return st;
+      b.q[j] = it.q;
+      b.out[j] = it.out;
+    }
+    b.n = n;
+    const ff_cache_desc& d = cache->desc;
+    const int chunk_tokens = int(cache->layout.chunk_tokens);
+    const hipError_t e =
+        d.dtype == FF_DT_BF16
+            ? ff::launch_attention_bf16_batch(chunk_tokens, d.num_heads, d.head_dim, softmax_scale,
+                                              b, static_cast<hipStream_t>(stream))
+            : ff::launch_attention_f32_batch(chunk_tokens, d.num_heads, d.head_dim, softmax_scale,
+                                             b, static_cast<hipStream_t>(stream));
+    return hip_status(e, "chunk_attention_batch launch");
   });
 }
 

@@ -33,6 +33,16 @@ struct KvSegments {
   int32_t total;  // sum of len
 };
 
+// Read sets of a batched launch (ff_chunk_attention_batch): the queries of
+// item j (q[j], out[j], [nq][heads][d] each) read set[j].
+constexpr int kMaxBatch = FF_MAX_BATCH;
+struct KvBatch {
+  KvSegments set[kMaxBatch];
+  const void* q[kMaxBatch];
+  void* out[kMaxBatch];
+  int32_t n;
+};
+
 // Read sets of a packed launch (ff_packed_attention): one stage's chunks
 // 0 .. n_chunks-1 in one token-major array, and anchor frames in another.
 // Chunk c reads its anchor frames, grouped into runs of consecutive frames
@@ -126,6 +136,13 @@ hipError_t launch_attention_bf16(const void* q, void* out, int nq, int heads, in
 hipError_t launch_attention_f32(const void* q, void* out, int nq, int heads, int head_dim,
                                 float softmax_scale, const KvSegments& segs,
                                 hipStream_t stream);
+
+// Batched launches: item j of b reads b.set[j]; no tail split.
+hipError_t launch_attention_bf16_batch(int nq, int heads, int head_dim, float softmax_scale,
+                                       const KvBatch& b, hipStream_t stream);
+
+hipError_t launch_attention_f32_batch(int nq, int heads, int head_dim, float softmax_scale,
+                                      const KvBatch& b, hipStream_t stream);
 
 // Packed launches: q and out are [n_chunks * chunk_tokens][heads][d]; the
 // queries of chunk c read packed_segment(plan, c, .).

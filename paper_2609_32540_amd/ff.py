@@ -25,7 +25,8 @@ MAX_RING_CHUNKS = 8
 MAX_ANCHOR_FRAMES = 8
 MAX_ROPE_FRAMES = 16
 MAX_PACKED_CHUNKS = 128
-ABI_VERSION = 2
+MAX_BATCH = 4
+ABI_VERSION = 3
 
 
 class FFError(RuntimeError):
@@ -59,6 +60,16 @@ class PackedDesc(ctypes.Structure):
     ]
 
 
+class AttentionItem(ctypes.Structure):
+    _fields_ = [
+        ("stage", ctypes.c_int32), ("layer", ctypes.c_int32), ("chunk_index", ctypes.c_int64),
+        ("q", ctypes.c_void_p), ("k_cur", ctypes.c_void_p), ("v_cur", ctypes.c_void_p),
+        ("out", ctypes.c_void_p), ("bank_k", ctypes.c_void_p), ("bank_v", ctypes.c_void_p),
+        ("n_frames", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("frame_index", ctypes.POINTER(ctypes.c_int32)),
+    ]
+
+
 # int32_t (*ff_stage_forward_fn)(void* user, int32_t stage, int64_t chunk, void* stream)
 STAGE_FORWARD_FN = ctypes.CFUNCTYPE(ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                     ctypes.c_int64, ctypes.c_void_p)
@@ -77,6 +88,8 @@ SIGNATURES = [
     ("ff_chunk_attention", _I32, [_VP, _I32, _I32, _I64, _VP, _VP, _VP, _VP, ctypes.c_float, _VP]),
     ("ff_chunk_attention_bank", _I32, [_VP, _I32, _I32, _I64, _VP, _VP, _VP, _VP, ctypes.c_float,
                                        _VP, _VP, _I32, _PI32, _VP]),
+    ("ff_chunk_attention_batch", _I32, [_VP, _I32, ctypes.POINTER(AttentionItem), ctypes.c_float,
+                                        _VP]),
     ("ff_cache_ring_state", _I32, [_VP, _I32, _I32, _PI64, _PI64]),
     ("ff_cache_anchor_state", _I32, [_VP, _I32, _PI32, _PI32]),
     ("ff_cache_read", _I32, [_VP, _I32, _I32, _I32, _VP, _VP, _VP]),
@@ -255,6 +268,45 @@ class RendererCache:
                                              ctypes.c_float(scale), bk, bv, len(frames), fr,
                                              _stream_handle(self.device, stream)))
         return out
+
+    def chunk_attention_batch(self, items: Sequence[dict], scale: Optional[float] = None,
+                              stream: Optional[torch.cuda.Stream] = None) -> List[torch.Tensor]:
+        """ff_chunk_attention_batch: up to MAX_BATCH attention calls in one launch.  Each
+        item is a dict with stage, layer, chunk, q, k, v and optionally out, and bank_k,
+        bank_v, frames for the bank path; returns the outputs in item order."""
+        if not 1 <= len(items) <= MAX_BATCH:
+            raise ValueError(f"1 .. {MAX_BATCH} items per batch, got {len(items)}")
+        arr = (AttentionItem * len(items))()
+        outs, keep = [], []
+        for j, it in enumerate(items):
+            a = arr[j]
+            a.stage, a.layer, a.chunk_index = it["stage"], it["layer"], it["chunk"]
+            a.q = self._tensor(it["q"], self.chunk_tokens, "q")
+            a.k_cur = self._tensor(it["k"], self.chunk_tokens, "k")
+            a.v_cur = self._tensor(it["v"], self.chunk_tokens, "v")
+            out = it.get("out")
+            if out is None:
+                out = torch.empty_like(it["q"])
+            a.out = self._tensor(out, self.chunk_tokens, "out")
+            outs.append(out)
+            if it.get("bank_k") is not None:
+                bank_k, bank_v, frames = it["bank_k"], it["bank_v"], list(it["frames"])
+                if bank_k.shape[0] % self.tokens_per_frame:
+                    raise ValueError("the bank must hold whole frames")
+                a.bank_k = self._tensor(bank_k, bank_k.shape[0], "bank_k")
+                a.bank_v = self._tensor(bank_v, bank_k.shape[0], "bank_v")
+                n_bank = bank_k.shape[0] // self.tokens_per_frame
+                if any(not 0 <= f < n_bank for f in frames):
+                    raise ValueError(f"bank frame index out of range [0, {n_bank})")
+                fr = (ctypes.c_int32 * max(len(frames), 1))(*frames)
+                keep.append(fr)
+                a.n_frames = len(frames)
+                a.frame_index = ctypes.cast(fr, ctypes.POINTER(ctypes.c_int32))
+        if scale is None:
+            scale = 1.0 / math.sqrt(self.head_dim)
+        _check(lib().ff_chunk_attention_batch(self._h, len(items), arr, ctypes.c_float(scale),
+                                              _stream_handle(self.device, stream)))
+        return outs
 
     # ------------------------------------------------------------------
     def ring_state(self, stage: int, layer: int) -> Tuple[List[int], int]:

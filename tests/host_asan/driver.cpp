@@ -83,6 +83,26 @@ static void ring_sequences() {
                                            nullptr) == FF_ERR_INVALID_ARG);
             if (c > 5)   // the first publish of a ring may start at any chunk
               EXPECT(ff_kv_publish(h, s, l, c + 1, t, t, nullptr) == FF_ERR_ORDER);
+            // the same call as one item of a batch, beside a bank item and a duplicate
+            ff_attention_item items[FF_MAX_BATCH + 1] = {};
+            for (int j = 0; j <= FF_MAX_BATCH; ++j) {
+              items[j].stage = s;
+              items[j].layer = l;
+              items[j].chunk_index = c;
+              items[j].q = items[j].k_cur = items[j].v_cur = t;
+              items[j].out = t;
+            }
+            items[1].bank_k = items[1].bank_v = t;
+            items[1].n_frames = 5;
+            items[1].frame_index = frames;
+            EXPECT(ff_chunk_attention_batch(h, 2, items, 0.125f, nullptr) == FF_OK);
+            EXPECT(ff_chunk_attention_batch(h, FF_MAX_BATCH, items, 0.125f, nullptr) == FF_OK);
+            EXPECT(ff_chunk_attention_batch(h, FF_MAX_BATCH + 1, items, 0.125f, nullptr) ==
+                   FF_ERR_UNSUPPORTED);
+            EXPECT(ff_chunk_attention_batch(h, 0, items, 0.125f, nullptr) == FF_ERR_UNSUPPORTED);
+            items[2].chunk_index = c + 1;   // out of order: the whole batch is refused
+            if (c > 5)                      // (an empty ring accepts any chunk)
+              EXPECT(ff_chunk_attention_batch(h, 3, items, 0.125f, nullptr) == FF_ERR_ORDER);
             EXPECT(ff_kv_publish(h, s, l, c, t, t, nullptr) == FF_OK);
             std::vector<int64_t> slots(W, -2);
             int64_t count = -1;

@@ -73,6 +73,19 @@ hipError_t launch_attention_f32(const void* q, void* out, int nq, int heads, int
                segments_ok(segs));
 }
 
+hipError_t launch_attention_bf16_batch(int nq, int heads, int head_dim, float, const KvBatch& b,
+                                       hipStream_t) {
+  bool ok = nq > 0 && heads > 0 && (head_dim == 64 || head_dim == 128) && b.n >= 1 &&
+            b.n <= kMaxBatch;
+  for (int j = 0; ok && j < b.n; ++j) ok = b.q[j] && b.out[j] && segments_ok(b.set[j]);
+  return check(ok);
+}
+
+hipError_t launch_attention_f32_batch(int nq, int heads, int head_dim, float scale,
+                                      const KvBatch& b, hipStream_t stream) {
+  return launch_attention_bf16_batch(nq, heads, head_dim, scale, b, stream);
+}
+
 namespace {
 bool plan_ok(const PackedPlan& p, int heads, int head_dim, int elem) {
   if (p.n_chunks < 1 || p.n_chunks > FF_MAX_PACKED_CHUNKS || p.chunk_tokens < 1) return false;

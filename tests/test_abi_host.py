@@ -34,11 +34,11 @@ def desc(**kw):
 def test_library_exports_every_header_symbol():
     L = ff.lib()
     names = header_functions()
-    assert len(names) == 21
+    assert len(names) == 22
     for n in names:
         assert hasattr(L, n), n
     assert {n for n, _, _ in ff.SIGNATURES} == set(names)
-    assert L.ff_abi_version() == ff.ABI_VERSION == 2
+    assert L.ff_abi_version() == ff.ABI_VERSION == 3
 
 
 def test_cache_bytes_layout():

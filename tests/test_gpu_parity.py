@@ -277,6 +277,48 @@ def test_attention_running_max_rescales(head_dim, heads, grid):
         hist = (hist + [(exact(k), exact(v))])[-W:]
 
 
+@pytest.mark.parametrize("dtype,head_dim", [("bf16", 128), ("bf16", 64), ("f32", 64)])
+def test_attention_batch_equals_single_calls(dtype, head_dim):
+    # the rounds of a 4-stage wavefront (round n: chunk n - s at stage s), each
+    # round's attention as one ff_chunk_attention_batch; stage 3 reads its anchors
+    # from a bank.  Bit-identical to the single calls (the batch is never split
+    # along keys, and no single call here is), and within the bar of the oracle.
+    S = 4
+    w = small(dtype, head_dim, heads=3, ring_chunks=2, stages=S, layers=1, n_chunks=5,
+              anchor_rule="fixed:0,7", max_anchor_frames=2)
+    ca, cb = make_cache(w, S, 1), make_cache(w, S, 1)
+    frames = [0, 7]
+    ak, av = synth.anchor_tensors(w, frames, 0)
+    akd, avd = to_dev(ak), to_dev(av)
+    for c in (ca, cb):
+        c.anchor_set(0, frames, akd, avd)
+    oracle = make_oracle(w, S, 1)
+    oracle.anchor_set(0, frames, exact(ak), exact(av))
+    scale = 1.0 / math.sqrt(head_dim)
+    for n in range(w.n_chunks + S - 1):
+        work = [(s, n - s) for s in range(S) if 0 <= n - s < w.n_chunks]
+        items, singles, tensors = [], [], []
+        for s, i in work:
+            q, k, v = (to_dev(synth.chunk_tensor(w, t, i, s, 0))
+                       for t in (synth.T_Q, synth.T_K, synth.T_V))
+            tensors.append((s, i, q, k, v))
+            it = dict(stage=s, layer=0, chunk=i, q=q, k=k, v=v)
+            if s == 3:
+                it.update(bank_k=akd, bank_v=avd, frames=[1, 0])
+                singles.append(cb.chunk_attention_bank(s, 0, i, q, k, v, akd, avd, [1, 0]))
+            else:
+                singles.append(cb.chunk_attention(s, 0, i, q, k, v))
+            items.append(it)
+        outs = ca.chunk_attention_batch(items, scale=scale)
+        for (s, i, q, k, v), o, o1 in zip(tensors, outs, singles):
+            assert torch.equal(o, o1), (n, s, i)
+            ref = oracle.attention(s, 0, i, exact(q), exact(k), exact(v), scale=scale)
+            check_attention(exact(o), ref, dtype, f"round {n} stage {s} chunk {i}")
+            for c in (ca, cb):
+                c.kv_publish(s, 0, i, k, v)
+            oracle.publish(s, 0, i, exact(k), exact(v))
+
+
 def test_unfilled_slots_poisoned_with_nan_are_never_read():
     w = small("bf16", 128, ring_chunks=4, anchor_rule="fixed:3", max_anchor_frames=3)
     run = PairedRun(w, poison=True)
