@@ -268,8 +268,30 @@ def wavefront_clip(name: str = "1.3b-480p") -> dict:
                 kk = S - s
                 ff.euler_step(x, h, sig[kk] - sig[kk - 1], out=x, stream=stream)
 
+        def batched_round(n, stream):
+            # the round's forwards on one stream, their attention as one launch
+            work = [(s, n - s) for s in range(S) if 0 <= n - s < N_R]
+            with torch.cuda.stream(stream):
+                items = []
+                for s, i in work:
+                    x = X[i]
+                    q, k, v = x.clone(), (x * 0.5).to(x.dtype), (x + 0.25).to(x.dtype)
+                    cache.rope3d(q, k, [w.frames_per_chunk * i + f for f in range(w.frames_per_chunk)],
+                                 stream=stream)
+                    items.append(dict(stage=s, layer=0, chunk=i, q=q, k=k, v=v, bank_k=bank_k,
+                                      bank_v=bank_v, frames=windows[i]))
+                outs = cache.chunk_attention_batch(items, stream=stream)
+                for (s, i), it, h in zip(work, items, outs):
+                    cache.kv_publish(s, 0, i, it["k"], it["v"], stream=stream)
+                    kk = S - s
+                    ff.euler_step(X[i], h, sig[kk] - sig[kk - 1], out=X[i], stream=stream)
+
         t0 = time.perf_counter()
-        if len(streams) == 1:
+        if streams == "batched":
+            for n in range(N_R + S - 1):
+                batched_round(n, one[0])
+            rounds, fwd = N_R + S - 1, N_R * S
+        elif len(streams) == 1:
             for i in range(N_R):
                 for s in range(S):
                     forward(s, i, streams[0])
@@ -285,15 +307,21 @@ def wavefront_clip(name: str = "1.3b-480p") -> dict:
     many = [torch.cuda.Stream() for _ in range(S)]
     run(one)                                   # warm: code objects and each stream's
     run(many)                                  # pool of the caching allocator
+    run("batched")
     t_seq, _, _, X_seq = run(one)
     t_wave, rounds, fwd, X_wave = run(many)
+    t_bat, _, _, X_bat = run("batched")
     same = all(torch.equal(a, b) for a, b in zip(X_seq, X_wave))
-    log(f"wavefront {name}: {rounds} rounds, {fwd} forwards, {t_wave * 1e3:.1f} ms on {S} streams "
-        f"vs {t_seq * 1e3:.1f} ms chunk-major on one stream; identical latents: {same}")
+    same_b = all(torch.equal(a, b) for a, b in zip(X_seq, X_bat))
+    log(f"wavefront {name}: {rounds} rounds, {fwd} forwards, {t_wave * 1e3:.1f} ms on {S} streams, "
+        f"{t_bat * 1e3:.1f} ms with each round's attention batched on one stream, vs "
+        f"{t_seq * 1e3:.1f} ms chunk-major on one stream; identical latents: {same and same_b}")
     return {"workload": name, "layers": 1, "stages": S, "chunks": N_R, "rounds": rounds,
             "forwards": fwd, "ms_wavefront_streams": round(t_wave * 1e3, 2),
+            "ms_wavefront_batched_rounds": round(t_bat * 1e3, 2),
             "ms_chunk_major_one_stream": round(t_seq * 1e3, 2),
-            "speedup": round(t_seq / t_wave, 3), "latents_identical": bool(same)}
+            "speedup": round(t_seq / t_wave, 3), "speedup_batched": round(t_seq / t_bat, 3),
+            "latents_identical": bool(same and same_b)}
 
 
 def copy_calibration() -> int:
