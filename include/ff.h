@@ -221,10 +221,9 @@ typedef struct {
 
 /* The attention of 1 <= n <= FF_MAX_BATCH independent items in one launch,
  * e.g. the stages' forwards of one wavefront round (chunk i at stage s, chunk
- * i-1 at stage s+1, ..).  Items whose grids are small next to the GPU (far
- * fewer (head, 256-query) units than compute units) then share one round of
- * workgroups instead of taking one each; items that nearly fill the GPU gain
- * nothing.  Item j computes exactly what its ff_chunk_attention(_bank)
+ * i-1 at stage s+1, ..): one launch instead of n, which pays for items small
+ * next to the GPU (far fewer (head, 256-query) units than compute units).
+ * Item j computes exactly what its ff_chunk_attention(_bank)
  * call would, bit for bit: the batch is never split along keys (Sec. 3.1 and
  * App. Alg. 1, the Evaluate step of every rank of a round).  Items share
  * softmax_scale; each is validated as its single call would be, all before
