@@ -3,41 +3,44 @@
 // Work split: a workgroup = 8 waves = 256 queries of one head, one workgroup
 // per CU (two waves per SIMD); each wave owns 32 queries for the whole key
 // loop.  Keys arrive as segments (anchor segment, valid history slots, current
-// chunk);
-// each segment is cut into 64-key tiles and only a segment's last tile is
-// partial (its missing keys are masked to -inf): no tile straddles two
+// chunk); each segment is cut into 64-key tiles and only a segment's last tile
+// is partial (its missing keys are masked to -inf): no tile straddles two
 // segments and no empty slot is touched.
 //
-// Products, per 64-key tile:
+// Products, per 32-key block (two per tile):
 //   S^T = K Q^T     v_mfma_f32_32x32x16_bf16; A = K rows read from LDS, B = the
 //                   wave's Q^T, held in registers for the whole loop.
 //   softmax         the accumulator layout of S^T puts one query column in each
 //                   lane (half of a 32-key block; the other half is in lane ^ 32),
-//                   so max and sum are in-lane plus one v_permlane32_swap.  exp2
-//                   with log2(e) folded into the scale.  The running max is only
-//                   raised (and O rescaled) when a column max exceeds it by more
-//                   than 8 (log2 units, probabilities up to 2^8); otherwise the
-//                   stale max stays the reference, which leaves the result exact
-//                   since the final sum uses the same max.
+//                   so the row sums stay in-lane until the end.  p = exp2(s c -
+//                   m) with c = scale * log2 e applied in float32 (one fma; Q is
+//                   not rounded again after scaling).  The reference max m is the
+//                   first block's column max and is only raised when a block's
+//                   probabilities sum past kSumLimit (every kept probability is
+//                   then at most kSumLimit, and infinities from scores far above
+//                   the reference trip the same test): that rare block is
+//                   recomputed from LDS, O and l rescaled and its probabilities
+//                   redone.  The result is exact for any reference, since the
+//                   final sum uses the same one; no column max is taken per block.
 //   O^T += V^T P^T  A = V^T, read from the row-major V tile with the gfx950
 //                   transposing LDS read (ds_read_b64_tr_b16); B = P^T, the
 //                   softmax registers rounded to bf16 in place.  The keys of each
 //                   8-key operand are chosen to match the accumulator layout.
-// Software pipeline: h1(t) computes block 0 of S^T of tile t+1 on the matrix
-// core beside the exponentials of tile t, then O^T += block 0 of tile t;
-// h2(t) computes block 1 of S^T(t+1), O^T += block 1 of tile t and the column
-// max of tile t+1.  Waves w and
-// w + 4 share a SIMD: waves 0-3 run h1(t) h2(t) after barrier t, waves 4-7 run
-// h2(t-1) h1(t), half an iteration later, so on every SIMD one wave's
-// exponentials run beside the other's matrix work instead of both waves
-// wanting the same unit at once.
+// Software pipeline over blocks b: A(b) computes S^T of block b+1 on the matrix
+// core beside the exponentials of block b; B(b) checks block b's sum, adds
+// block b into O^T and masks block b+1 if it is partial.  Waves w and w + 4
+// share a SIMD: waves 0-3 run A(2t) B(2t) A(2t+1) B(2t+1) after barrier t,
+// waves 4-7 run one phase later, B(2t-1) A(2t) B(2t) A(2t+1), so on every SIMD
+// one wave's exponentials run beside the other's matrix work.
 // K and V tiles are copied from HBM straight into LDS (global_load_lds_dwordx4,
-// 16 bytes per lane, issued by waves 0-3) two tiles ahead, into a ring of four
-// tile slots: one barrier per tile (plus one at the end).  The last reads of
-// tile t (h2(t) of waves 4-7) come before barrier t+2, where tile t+4 is
-// copied into its slot.  The loops are unrolled by four so every slot
-// reference is static (reads of one slot are never ordered behind the copy
-// into another).
+// 16 bytes per lane) by waves 0-3 at the end of their step t, three tiles
+// ahead, into a ring of five tile slots (all 160 KB of LDS at d = 128): the
+// slot of tile t+3 held tile t-2, whose last read (waves 4-7, B(2t-3)) came
+// before barrier t.  Barrier t waits only for the copy of tile t+1, so each
+// copy has a whole step to land.  The copies are issued from inline assembly
+// and waited for explicitly, so the compiler does not add its own conservative
+// waits for them; the loops are unrolled by five so every slot reference is
+// static.
 // Tile rows are stored without padding, with an XOR swizzle of their 16-byte
 // chunks that keeps both the K reads and the transposing V reads free of bank
 // conflicts on the 64-bank LDS.
@@ -77,7 +80,7 @@ constexpr int kWaveQ = 32 * kCB;            // queries per wave
 constexpr int kBlockQ = kWaves * kWaveQ;    // queries per workgroup
 constexpr int kBK = 64;                     // keys per tile
 constexpr int kXcds = 8;
-constexpr float kRescaleThreshold = 8.0f;   // log2 units
+constexpr float kSumLimit = 16.0f;          // largest block sum of probabilities kept
 // Waves w and w + 4 share a SIMD and the issue arbiter favours the older one
 // (w < 4), which reaches each tile's barrier well ahead of its partner; the
 // tile copies are therefore all issued by waves 0-3, off the partner's path.
@@ -109,6 +112,15 @@ template <int D>
 __device__ inline int swz(int r) {
   if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
   else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
+
+// 16 bytes per lane from global memory (uniform base + per-lane byte offset)
+// straight into LDS at dst + 16 * lane.  Written out so that the compiler does
+// not track these copies: their completion is waited for explicitly (vmcnt)
+// before the barrier that hands a tile to the other waves.
+__device__ inline void lds_copy16(uint32_t dst, const char* base, uint32_t off) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(dst), "v"(off), "s"(base) : "memory");
 }
 
 __device__ inline uint32_t pack_bf16(float a, float b) {
@@ -154,6 +166,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
   __shared__ __attribute__((aligned(1024))) char lds2[C::SLOT];
   __shared__ __attribute__((aligned(1024))) char lds3[C::SLOT];
+  __shared__ __attribute__((aligned(1024))) char lds4[C::SLOT];
 
   // Workgroups b < tail.n_full run whole units (head, 256-query tile),
   // renumbered XCD-aware: hardware block b runs on XCD b % 8, so each XCD gets
@@ -202,7 +215,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   const int qt = rest % n_qtiles;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform
   const int lane = tid & 63;
   const int l32 = lane & 31;
   const int half = lane >> 5;
@@ -216,7 +229,11 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     const int qi = min(q0 + 32 * cb + l32, nq - 1);
     const __bf16* qp = q + (int64_t(qi) * heads + head) * D + 8 * half;
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s) qreg[cb][s] = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
+    for (int s = 0; s < C::KS; ++s) {
+      typedef float f32x8 __attribute__((ext_vector_type(8)));
+      const bf16x8 raw = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
+      qreg[cb][s] = raw;
+    }
   }
 
   f32x16 o[kCB][C::DB];
@@ -229,7 +246,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   float m_run[kCB], l_run[kCB];
 #pragma unroll
   for (int cb = 0; cb < kCB; ++cb) {
-    m_run[cb] = -INFINITY;  // running max of scaled logits (log2 units)
+    m_run[cb] = 0.0f;       // reference max of the scaled logits (log2 units)
     l_run[cb] = 0.0f;       // this lane's partial sum of probabilities
   }
 
@@ -264,7 +281,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   // this workgroup's share of the tiles: [t_begin, t_begin + n_tiles)
   const int t_begin = part_id * n_tiles / n_parts;
   n_tiles = (part_id + 1) * n_tiles / n_parts - t_begin;
-  auto advance = [&](Cursor c) {
+  auto advance = [&](Cursor c) __attribute__((always_inline)) {
     c.k0 += kBK;
     if (c.k0 >= seg_len(c.sg)) {
       ++c.sg;
@@ -285,7 +302,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     cp_row[i] = r;
     cp_choff[i] = 16 * ((lane % C::CPR) ^ swz<D>(r));
   }
-  auto issue_tile = [&](char* base, Cursor c) {
+  auto issue_tile = [&](char* base, Cursor c) __attribute__((always_inline)) {
     if (wave >= kCopyWaves) return;
     const int len = seg_len(c.sg);
     const uint32_t row_bytes = uint32_t(__builtin_amdgcn_readlane(int(sg_row_bytes), c.sg));
@@ -297,9 +314,9 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       int tok = c.k0 + cp_row[i];
       if (partial) tok = min(tok, len - 1);
       const uint32_t off = uint32_t(tok) * row_bytes + uint32_t(cp_choff[i]);
-      char* dst = base + (wave * C::BLOCKS_PER_WAVE + i) * 1024;
-      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(kb + off), LDS_PTR(void, dst), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(vb + off), LDS_PTR(void, dst + C::TILE), 16, 0, 0);
+      const uint32_t dst = uint32_t(size_t(LDS_PTR(char, base))) + (wave * C::BLOCKS_PER_WAVE + i) * 1024;
+      lds_copy16(dst, kb, off);
+      lds_copy16(dst + C::TILE, vb, off);
     }
   };
 
@@ -325,76 +342,84 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   // chunk bits flipped per d block: D = 128 has 4 chunks per 32-d block, D = 64 as well
   constexpr int kVdbShift = 6;   // (4 chunks per db) << 4 bytes
 
-  // S^T of 32-key block kb of a tile into s[kb][cb], both column blocks
-  auto compute_s = [&](const char* kt, int kb, f32x16 (&s)[2][kCB]) {
-#pragma unroll
-    for (int cb = 0; cb < kCB; ++cb)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) s[kb][cb][j] = 0.0f;
+  // S^T of 32-key block kb of the tile at kt, both column blocks
+  auto s_blk = [&](const char* kt, int kb, f32x16 (&s)[kCB]) __attribute__((always_inline)) {
     const char* kbase = kt + kb * 32 * C::ROWB;
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks) {
       const bf16x8 a = *reinterpret_cast<const bf16x8*>(kbase + (k_lane ^ (ks << 5)));
 #pragma unroll
       for (int cb = 0; cb < kCB; ++cb)
-        s[kb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[cb][ks], s[kb][cb], 0, 0, 0);
+        s[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[cb][ks], ks == 0 ? f32x16{} : s[cb],
+                                                        0, 0, 0);
     }
   };
-
-  // mask keys >= n_valid of a partial tile (register j of block kb holds key
-  // kb*32 + 8 (j / 4) + 4 half + j % 4)
-  auto mask_s = [&](f32x16 (&s)[2][kCB], int n_valid) {
+  // mask keys >= n_valid of a 32-key block (register j holds key 8 (j / 4) + 4 half + j % 4)
+  auto mask_blk = [&](f32x16 (&s)[kCB], int n_valid) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int cb = 0; cb < kCB; ++cb)
 #pragma unroll
       for (int j = 0; j < 16; ++j)
-        if (kb * 32 + 8 * (j >> 2) + 4 * half + (j & 3) >= n_valid)
-#pragma unroll
-          for (int cb = 0; cb < kCB; ++cb) s[kb][cb][j] = -INFINITY;
+        s[cb][j] = 8 * (j >> 2) + 4 * half + (j & 3) >= n_valid ? -INFINITY : s[cb][j];
   };
-
-  // column max of a tile; raise the running max (and rescale O) when it grows
-  // by more than the threshold
-  auto update_max = [&](const f32x16 (&s)[2][kCB]) {
+  // reference max from the first block: its column max (O and l are still zero)
+  auto first_max = [&](const f32x16 (&s)[kCB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int cb = 0; cb < kCB; ++cb) {
-      float mx = s[0][cb][0];
+      float mx = s[cb][0];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[kb][cb][j]);
-      mx = max_across_halves(mx) * scale_log2;
-      if (__builtin_amdgcn_ballot_w64(mx > m_run[cb] + kRescaleThreshold) != 0) {
-        const float m_new = fmaxf(m_run[cb], mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_run[cb] - m_new);
-        m_run[cb] = m_new;
-        l_run[cb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) o[cb][db][j] *= alpha;
-      }
+      for (int j = 1; j < 16; ++j) mx = fmaxf(mx, s[cb][j]);
+      m_run[cb] = max_across_halves(mx) * scale_log2;
     }
   };
-
-  // probabilities of 32-key block kb, both column blocks, as packed bf16
-  auto probs = [&](const f32x16 (&s)[2][kCB], int kb, uint32_t (&pk)[kCB][8]) {
+  // probabilities of a block as packed bf16
+  auto p_blk = [&](const f32x16 (&s)[kCB], uint32_t (&pk)[kCB][8], float (&lb)[kCB])
+      __attribute__((always_inline)) {
 #pragma unroll
     for (int cb = 0; cb < kCB; ++cb) {
-      float sum = 0.0f;
+      float sum = -0.0f;
 #pragma unroll
       for (int j = 0; j < 16; j += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kb][cb][j], scale_log2, -m_run[cb]));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kb][cb][j + 1], scale_log2, -m_run[cb]));
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[cb][j], scale_log2, -m_run[cb]));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[cb][j + 1], scale_log2, -m_run[cb]));
         sum += p0 + p1;
         pk[cb][j >> 1] = pack_bf16(p0, p1);
       }
-      l_run[cb] += sum;
+      lb[cb] = sum;
     }
   };
-
-  // O^T += V^T P^T for 32-key block kb
-  auto pv = [&](const char* vt, int kb, const uint32_t (&pk)[kCB][8]) {
+  // The reference max is only raised when a block's probabilities (relative to
+  // it) sum past kSumLimit: then this block's S^T is recomputed from LDS, the
+  // reference raised to its column max (O and l follow) and its probabilities
+  // redone.  Below the limit every probability is at most kSumLimit, so nothing
+  // overflows; infinities (scores far above the reference) also exceed it.
+  auto check_blk = [&](const char* kt, int kb, int nv_blk, uint32_t (&pk)[kCB][8], float (&lb)[kCB])
+      __attribute__((always_inline)) {
+    bool over = false;
+#pragma unroll
+    for (int cb = 0; cb < kCB; ++cb) over |= lb[cb] > kSumLimit;
+    if (__builtin_amdgcn_ballot_w64(over) == 0) return;
+    f32x16 sr[kCB];
+    s_blk(kt, kb, sr);
+    if (nv_blk < 32) mask_blk(sr, nv_blk);
+#pragma unroll
+    for (int cb = 0; cb < kCB; ++cb) {
+      float mx = sr[cb][0];
+#pragma unroll
+      for (int j = 1; j < 16; ++j) mx = fmaxf(mx, sr[cb][j]);
+      const float m_new = fmaxf(m_run[cb], max_across_halves(mx) * scale_log2);
+      const float alpha = __builtin_amdgcn_exp2f(m_run[cb] - m_new);
+      l_run[cb] *= alpha;
+#pragma unroll
+      for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) o[cb][db][j] *= alpha;
+      m_run[cb] = m_new;
+    }
+    p_blk(sr, pk, lb);
+  };
+  // O^T += V^T P^T for 32-key block kb of the tile at vt
+  auto pv_blk = [&](const char* vt, int kb, const uint32_t (&pk)[kCB][8]) __attribute__((always_inline)) {
 #pragma unroll
     for (int mh = 0; mh < 2; ++mh) {
       bf16x8 pb[kCB];
@@ -407,7 +432,6 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       const char* vbase = vt + (kb * 32 + 16 * mh) * C::ROWB;
 #pragma unroll
       for (int db = 0; db < C::DB; ++db) {
-        // keys kbase .. +3 (lo) and kbase + 8 .. +11 (hi) of this 16-key group
         const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             LDS_PTR(s16x4, vbase + (v_lane[0] ^ (db << kVdbShift))));
         const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -422,103 +446,129 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     }
   };
 
-  // ---- prologue: tiles 0 and 1 in flight, S^T of tile 0 -----------------------------
-  Cursor c_next = {0, 0};                    // the tile whose S^T the iteration computes
-  for (int i = 0; i < t_begin; ++i) c_next = advance(c_next);
-  Cursor c_dma = advance(c_next);            // the tile the iteration copies
-  issue_tile(lds0, c_next);
+  // ---- prologue: tiles 0 and 1 in flight, S^T of block 0 of tile 0 ----------------
+  Cursor c_s = {0, 0};                       // the tile of the S^T block being computed
+  for (int i = 0; i < t_begin; ++i) c_s = advance(c_s);
+  Cursor c_dma = advance(c_s);               // the tile the next copy fetches
+  issue_tile(lds0, c_s);
   if (n_tiles > 1) {
     issue_tile(lds1, c_dma);
     c_dma = advance(c_dma);                  // tile 2
   }
-  // S^T of even tiles lives in s_a, of odd tiles in s_b (no copies between them)
-  f32x16 s_a[2][kCB], s_b[2][kCB];
+  if (n_tiles > 2) {
+    issue_tile(lds2, c_dma);
+    c_dma = advance(c_dma);                  // tile 3
+  }
+  // S^T of even blocks (block 0 of a tile) lives in s_a, of odd blocks in s_b
+  f32x16 s_a[kCB], s_b[kCB];
+  uint32_t pk[kCB][8];
+  float lb[kCB];
+  int nv_s = min(kBK, seg_len(c_s.sg) - c_s.k0);   // valid keys of tile c_s
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  compute_s(lds0, 0, s_a);
-  compute_s(lds0, 1, s_a);
-  {
-    const int nv = min(kBK, seg_len(c_next.sg) - c_next.k0);
-    if (nv < kBK) mask_s(s_a, nv);
-  }
-  update_max(s_a);
-  c_next = advance(c_next);                  // tile 1
+  s_blk(lds0, 0, s_a);
+  if (nv_s < 32) mask_blk(s_a, nv_s);
+  first_max(s_a);
 
-  // ---- main loop, in two halves per tile ---------------------------------------
-  // h1(t): S^T block 0 of tile t+1, P^T of tile t, O^T += block 0 of tile t.
-  // h2(t): S^T block 1 of tile t+1, O^T += block 1 of tile t, column max of t+1.
-  // Waves 0-3 run [barrier t, copy of tile t+2, h1(t), h2(t)]; waves 4-7, which
-  // share their SIMDs, run half an iteration later, [barrier t, h2(t-1), h1(t)],
-  // so each SIMD pairs one wave's exponentials with the other's matrix work.
-  // Tile t lives in slot t % 4; the last reads of tile t (waves 4-7, h2(t))
-  // precede barrier t+2, where waves 0-3 copy tile t+4 into its slot.
-  uint32_t pk0[kCB][8], pk1[kCB][8];
-  auto h1 = [&](char* v_slot, char* k_slot, f32x16 (&s_cur)[2][kCB], f32x16 (&s_nxt)[2][kCB])
-      __attribute__((always_inline)) {
+  // ---- main loop over 32-key blocks -------------------------------------------
+  // Block b = 2t + kb is key block kb of tile t.  Phase A(b): S^T of block b+1
+  // on the matrix core beside the exponentials of block b.  Phase B(b): O^T +=
+  // block b beside the mask and column max of block b+1.  Waves 0-3 run
+  // [barrier t, copy of tile t+2, A(2t) B(2t) A(2t+1) B(2t+1)]; waves 4-7, which
+  // share their SIMDs, run one phase later, [barrier t, B(2t-1) A(2t) B(2t)
+  // A(2t+1)], so each SIMD pairs one wave's exponentials with the other's
+  // products.  Tile t lives in slot t % 4; the last read of tile t (waves 4-7,
+  // B(2t+1)) precedes barrier t+2, where waves 0-3 copy tile t+4 into its slot.
+  // A(2t):   s_b = S^T(tile t, block 1);   P of s_a.
+  // A(2t+1): s_a = S^T(tile t+1, block 0); P of s_b (only P for the last tile).
+  auto phA0 = [&](char* st) __attribute__((always_inline)) {
     asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
-    compute_s(k_slot, 0, s_nxt);
-    probs(s_cur, 0, pk0);
-    pv(v_slot + C::TILE, 0, pk0);
-    probs(s_cur, 1, pk1);
+    s_blk(st, 1, s_b);
+    p_blk(s_a, pk, lb);
   };
-  auto h2 = [&](int t, char* v_slot, char* k_slot, f32x16 (&s_nxt)[2][kCB])
-      __attribute__((always_inline)) {
+  auto phB0 = [&](char* st) __attribute__((always_inline)) {
     asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
-    compute_s(k_slot, 1, s_nxt);
-    pv(v_slot + C::TILE, 1, pk1);
+    check_blk(st, 0, nv_s, pk, lb);
+#pragma unroll
+    for (int cb = 0; cb < kCB; ++cb) l_run[cb] += lb[cb];
+    pv_blk(st + C::TILE, 0, pk);
+    if (nv_s < kBK) mask_blk(s_b, nv_s - 32);
+  };
+  auto phA1 = [&](int t, char* sn) __attribute__((always_inline)) {
+    asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
+    s_blk(sn, 0, s_a);   // (after the last tile: stale slot, result unused)
+    p_blk(s_b, pk, lb);
+  };
+  auto phB1 = [&](int t, char* st) __attribute__((always_inline)) {
+    asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
+    check_blk(st, 1, nv_s - 32, pk, lb);
+#pragma unroll
+    for (int cb = 0; cb < kCB; ++cb) l_run[cb] += lb[cb];
+    pv_blk(st + C::TILE, 1, pk);
     if (t + 1 < n_tiles) {
-      const int nv = min(kBK, seg_len(c_next.sg) - c_next.k0);
-      if (nv < kBK) mask_s(s_nxt, nv);
-      update_max(s_nxt);
-      c_next = advance(c_next);
+      c_s = advance(c_s);
+      nv_s = min(kBK, seg_len(c_s.sg) - c_s.k0);
+      if (nv_s < 32) mask_blk(s_a, nv_s);
     }
   };
-  // barrier t: every wave's copies of tile t+1 have landed, tile t-2 is free
-  auto sync = [&]() __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+  // barrier t: tile t+1 has landed (the copy of tile t+2, issued at the end of
+  // step t-1, may still be in flight) and every read of tile t-2 is done
+  auto sync = [&](int t) __attribute__((always_inline)) {
+    if (wave < kCopyWaves && t + 2 < n_tiles)
+      __builtin_amdgcn_s_waitcnt(2 * C::BLOCKS_PER_WAVE);   // vmcnt(copies of one tile), lgkmcnt(0)
+    else
+      __builtin_amdgcn_s_waitcnt(0);
+    asm volatile("s_barrier" ::: "memory");
   };
   if (wave < kCopyWaves) {
-    auto step = [&](int t, char* s0, char* s1, char* s2, f32x16 (&sc)[2][kCB],
-                    f32x16 (&sn)[2][kCB]) __attribute__((always_inline)) {
-      sync();
-      if (t + 2 < n_tiles) {
-        issue_tile(s2, c_dma);
+    // step t: A(2t) B(2t) A(2t+1) B(2t+1), then the copy of tile t+3 into the
+    // slot of tile t-2 (last read before barrier t)
+    auto step = [&](int t, char* s0, char* s1, char* s3) __attribute__((always_inline)) {
+      sync(t);
+      phA0(s0);
+      phB0(s0);
+      phA1(t, s1);
+      phB1(t, s0);
+      if (t + 3 < n_tiles) {
+        issue_tile(s3, c_dma);
         c_dma = advance(c_dma);
       }
-      h1(s0, s1, sc, sn);
-      h2(t, s0, s1, sn);
     };
     for (int t = 0; t < n_tiles;) {
-      step(t, lds0, lds1, lds2, s_a, s_b);
+      step(t, lds0, lds1, lds3);
       if (++t >= n_tiles) break;
-      step(t, lds1, lds2, lds3, s_b, s_a);
+      step(t, lds1, lds2, lds4);
       if (++t >= n_tiles) break;
-      step(t, lds2, lds3, lds0, s_a, s_b);
+      step(t, lds2, lds3, lds0);
       if (++t >= n_tiles) break;
-      step(t, lds3, lds0, lds1, s_b, s_a);
+      step(t, lds3, lds4, lds1);
+      if (++t >= n_tiles) break;
+      step(t, lds4, lds0, lds2);
       ++t;
     }
-    sync();   // matches the extra barrier of the last step of waves 4-7
+    sync(n_tiles);   // matches the extra barrier of the last step of waves 4-7
   } else {
-    sync();
-    h1(lds0, lds1, s_a, s_b);
-    // step t: barrier t, h2(t-1), and h1(t) while t < n_tiles; the step with
-    // t = n_tiles only finishes the last tile.  S^T of tile t is in sc.
-    auto step = [&](int t, char* sp, char* s0, char* s1, f32x16 (&sc)[2][kCB],
-                    f32x16 (&sn)[2][kCB]) __attribute__((always_inline)) {
-      sync();
-      h2(t - 1, sp, s0, sc);
-      if (t < n_tiles) h1(s0, s1, sc, sn);
+    // step t: barrier t, B(2t-1) (t > 0), then A(2t) B(2t) A(2t+1) while
+    // t < n_tiles; the step with t = n_tiles only finishes the last tile.
+    auto step = [&](int t, char* sp, char* s0, char* s1) __attribute__((always_inline)) {
+      sync(t);
+      if (t > 0) phB1(t - 1, sp);
+      if (t < n_tiles) {
+        phA0(s0);
+        phB0(s0);
+        phA1(t, s1);
+      }
     };
-    for (int t = 1;;) {
-      step(t, lds0, lds1, lds2, s_b, s_a);
+    for (int t = 0;;) {
+      step(t, lds4, lds0, lds1);
       if (t++ >= n_tiles) break;
-      step(t, lds1, lds2, lds3, s_a, s_b);
+      step(t, lds0, lds1, lds2);
       if (t++ >= n_tiles) break;
-      step(t, lds2, lds3, lds0, s_b, s_a);
+      step(t, lds1, lds2, lds3);
       if (t++ >= n_tiles) break;
-      step(t, lds3, lds0, lds1, s_a, s_b);
+      step(t, lds2, lds3, lds4);
+      if (t++ >= n_tiles) break;
+      step(t, lds3, lds4, lds0);
       if (t++ >= n_tiles) break;
     }
   }
