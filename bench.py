@@ -47,6 +47,11 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E (published)
 ATTN_SOURCE = os.path.join(ROOT, "paper_2609_32540_amd", "csrc", "attn_bf16.hip")
 
 
+def frames_of(w: synth.Workload, i: int):
+    """Anchor frames chunk i reads under the workload's rule, from the library."""
+    return ff.anchor_frames(w.anchor_rule, i, w.frames_per_chunk, w.latent_frames)
+
+
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -90,7 +95,7 @@ class Workspace:
     def kv_tokens(self, chunk: int) -> int:
         w = self.w
         n_hist = min(chunk, w.ring_chunks)
-        return (len(w.anchor_frames_for_chunk(chunk)) * w.tokens_per_frame
+        return (len(frames_of(w, chunk)) * w.tokens_per_frame
                 + n_hist * w.chunk_tokens + w.chunk_tokens)
 
     def attn_flops(self, chunk: int) -> float:
@@ -101,7 +106,7 @@ class Workspace:
         """Enqueue one chunk-stage forward; returns its attention FLOPs (all layers)."""
         w = self.w
         chunk, stage = self.next
-        frames_a = w.anchor_frames_for_chunk(chunk)
+        frames_a = frames_of(w, chunk)
         n_a = len(frames_a) * w.tokens_per_frame
         new_window = frames_a != self.anchor_frames
         frames = [chunk * w.frames_per_chunk + f for f in range(w.frames_per_chunk)]
@@ -161,10 +166,10 @@ def packed_clip(w: synth.Workload, reps: int = 3, backward: bool = True) -> dict
     shape = (n * Nq, w.heads, w.head_dim)
     q, k, v = (torch.randn(shape, generator=g, device=dev).to(w.torch_dtype) for _ in range(3))
     out = torch.empty_like(q)
-    frames = sorted({f for c in range(n) for f in w.anchor_frames_for_chunk(c)})
+    frames = sorted({f for c in range(n) for f in frames_of(w, c)})
     a_shape = (max(len(frames), 1) * G, w.heads, w.head_dim)
     ak, av = (torch.randn(a_shape, generator=g, device=dev).to(w.torch_dtype) for _ in range(2))
-    table = [[frames.index(f) for f in w.anchor_frames_for_chunk(c)] for c in range(n)]
+    table = [[frames.index(f) for f in frames_of(w, c)] for c in range(n)]
     flops = sum(4.0 * Nq * (len(table[c]) * G + (c - max(0, c - w.ring_chunks) + 1) * Nq)
                 * w.head_dim * w.heads for c in range(n))
 
@@ -239,14 +244,14 @@ def wavefront_clip(name: str = "1.3b-480p") -> dict:
     dev = torch.device("cuda", 0)
     S, N_R, G = w.stages, w.n_chunks, w.tokens_per_frame
     sig = [1.0 - j / S for j in range(S, -1, -1)]   # sigma_0 = 0 .. sigma_S = 1
-    frames = sorted({f for i in range(N_R) for f in w.anchor_frames_for_chunk(i)})
+    frames = sorted({f for i in range(N_R) for f in frames_of(w, i)})
     g = torch.Generator(device=dev)
     g.manual_seed(3)
     bank_k = torch.randn((len(frames) * G, w.heads, w.head_dim), generator=g, device=dev).to(w.torch_dtype)
     bank_v = torch.randn_like(bank_k, dtype=torch.float32).to(w.torch_dtype)
     noise = [torch.randn((w.chunk_tokens, w.heads, w.head_dim), generator=g, device=dev)
              .to(w.torch_dtype) for _ in range(N_R)]
-    windows = [[frames.index(f) for f in w.anchor_frames_for_chunk(i)] for i in range(N_R)]
+    windows = [[frames.index(f) for f in frames_of(w, i)] for i in range(N_R)]
 
     def run(streams):
         cache = ff.RendererCache(stages=S, layers=1, ring_chunks=w.ring_chunks,
@@ -347,7 +352,7 @@ def cpu_baseline(w: synth.Workload, target_s: float = 12.0) -> dict:
     except Exception:
         threads = os.cpu_count() or 1
     chunk = w.ring_chunks + 1
-    nkv = (len(w.anchor_frames_for_chunk(chunk)) * w.tokens_per_frame
+    nkv = (len(frames_of(w, chunk)) * w.tokens_per_frame
            + w.ring_chunks * w.chunk_tokens + w.chunk_tokens)
     rows = 512
     d = w.head_dim

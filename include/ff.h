@@ -19,7 +19,8 @@
  * ff_packed_attention evaluates the same attention for every chunk of one
  * stage in a single launch (the renderer rows of the packed block-causal
  * training mask, App. "packed" SFT, Alg. 2), and ff_anchor_partition /
- * ff_anchor_window compute the planner-side index sets P and Gamma(i).
+ * ff_anchor_window / ff_anchor_flank compute the planner-side index sets P,
+ * Gamma(i) and the long-horizon anchor set of a chunk.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -60,7 +61,7 @@
 extern "C" {
 #endif
 
-#define FF_ABI_VERSION 3
+#define FF_ABI_VERSION 4
 #define FF_MAX_RING_CHUNKS 8     /* W <= 8 */
 #define FF_MAX_ANCHOR_FRAMES 8   /* anchor frames per layer */
 #define FF_MAX_BATCH 4           /* items per ff_chunk_attention_batch call */
@@ -87,8 +88,12 @@ typedef enum { FF_DT_BF16 = 0, FF_DT_F32 = 1 } ff_dtype;
  *   grid_h, grid_w    latent tokens per frame = grid_h * grid_w
  *   head_dim          64 or 128
  *   rope_pairs_*      rotation pairs of the t, h and w axes; their sum must be
- *                     head_dim / 2 (the Wan2.1 split is d/2 - 2*floor(d/6),
- *                     floor(d/6), floor(d/6))
+ *                     head_dim / 2.  All three 0 selects the split of the
+ *                     Wan2.1 backbone, (d/2 - 2*floor(d/6), floor(d/6),
+ *                     floor(d/6)) = (22, 21, 21) at d = 128 and (12, 10, 10)
+ *                     at d = 64 (the paper fixes no RoPE; this is the one
+ *                     place the library reads it); ff_cache_get_desc reports
+ *                     the split in use
  *   rope_theta        RoPE base (10000)
  *   dtype             ff_dtype of every tensor and of the cache contents   */
 typedef struct {
@@ -128,6 +133,10 @@ ff_status ff_cache_create(const ff_cache_desc* desc, void* dev_buf, size_t dev_b
 
 /* Free the host-side handle (device memory stays the caller's). NULL is a no-op. */
 ff_status ff_cache_destroy(ff_cache* cache);
+
+/* The descriptor the cache was created with, as it uses it (the RoPE split
+ * filled in when it was given as all zeros). */
+ff_status ff_cache_get_desc(const ff_cache* cache, ff_cache_desc* out);
 
 /* 3D RoPE, in place, on q and/or k (either may be NULL), each
  * [n_frames * grid_h * grid_w][heads][head_dim] of the cache dtype.  Frame f of
@@ -180,10 +189,29 @@ ff_status ff_anchor_set(ff_cache* cache, int32_t layer, int32_t n_frames, const 
  * work as key parts whose partial results go to a per-stage scratch region
  * of the cache buffer, merged by a second kernel on the same stream: calls of
  * one stage (any layer) that overlap in time on different streams race on
- * it, so order them on one stream (different stages are independent). */
+ * it, so order them on one stream (different stages are independent), or use
+ * ff_chunk_attention_ws with a workspace per concurrent call. */
 ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
                              const void* q, const void* k_cur, const void* v_cur, void* out,
                              float softmax_scale, void* stream);
+
+/* Device bytes of the workspace that lets ff_chunk_attention_ws split every
+ * launch of this cache as ff_chunk_attention would (0 for float32 caches,
+ * which never split; 0 and an error for a NULL cache). */
+size_t ff_chunk_attention_workspace_bytes(const ff_cache* cache);
+
+/* ff_chunk_attention with the tail-split partial results in a caller-owned
+ * workspace (device, 16-byte aligned, `workspace_bytes` bytes) instead of the
+ * cache's per-stage scratch region, so calls of one stage (e.g. two layers)
+ * may overlap on different streams as long as each has its own workspace.
+ * A workspace smaller than ff_chunk_attention_workspace_bytes() only limits
+ * the split (results stay within the same bar); NULL runs unsplit.  The
+ * workspace is the caller's until the call's work on `stream` is done.
+ * Everything else as ff_chunk_attention (Sec. 3.1). */
+ff_status ff_chunk_attention_ws(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
+                                const void* q, const void* k_cur, const void* v_cur, void* out,
+                                float softmax_scale, void* workspace, size_t workspace_bytes,
+                                void* stream);
 
 /* ff_chunk_attention with the anchor KV read from a caller-owned anchor bank
  * instead of the layer's anchor segment (the bank A of Sec. 3.1 / App. Alg. 1,
@@ -223,20 +251,25 @@ typedef struct {
  * e.g. the stages' forwards of one wavefront round (chunk i at stage s, chunk
  * i-1 at stage s+1, ..): one launch instead of n, which pays for items small
  * next to the GPU (far fewer (head, 256-query) units than compute units).
- * Item j computes exactly what its ff_chunk_attention(_bank)
- * call would, bit for bit: the batch is never split along keys (Sec. 3.1 and
- * App. Alg. 1, the Evaluate step of every rank of a round).  Items share
+ * Item j computes its ff_chunk_attention(_bank) call's attention (Sec. 3.1 and
+ * App. Alg. 1, the Evaluate step of every rank of a round); the batch is
+ * never split along keys, so an item is bit-identical to a single call that
+ * is not tail-split either, and within the same bf16 bar of the exact result
+ * as a single call that is (its partial results are merged in a different
+ * order).  Items share
  * softmax_scale; each is validated as its single call would be, all before
  * anything is enqueued.  Items may read the same ring; their outputs must not
  * overlap each other or any input. */
 ff_status ff_chunk_attention_batch(ff_cache* cache, int32_t n, const ff_attention_item* items,
                                    float softmax_scale, void* stream);
 
-/* Host bookkeeping of one ring: slot_chunk[s] (W entries, host) is the chunk
- * held by slot s or -1; *published_count is the next chunk the ring expects
- * (0 if nothing was published).  Either output may be NULL. */
+/* Host bookkeeping of one ring (Eq. step-update): slot_chunk[s] (W entries,
+ * host) is the chunk held by slot s or -1; *next_chunk is the chunk the ring
+ * expects next (-1 while nothing was published: any chunk may come first);
+ * *n_published counts the publishes so far (equal to *next_chunk when the
+ * first publish was chunk 0).  Any output may be NULL. */
 ff_status ff_cache_ring_state(const ff_cache* cache, int32_t stage, int32_t layer,
-                              int64_t* slot_chunk, int64_t* published_count);
+                              int64_t* slot_chunk, int64_t* next_chunk, int64_t* n_published);
 
 /* Anchor bookkeeping of one layer: *n_frames and frame_t[0 .. n_frames)
  * (room for max_anchor_frames values).  Either output may be NULL. */
@@ -339,6 +372,17 @@ ff_status ff_anchor_partition(int32_t L, int32_t delta, int32_t* out, int32_t ca
  * Host only. */
 ff_status ff_anchor_window(int64_t i, int32_t frames_per_chunk, int32_t delta, int32_t L,
                            int32_t* out3, int32_t* n_out);
+
+/* Long-horizon anchor set of renderer chunk i: the first-frame anchor and the
+ * two anchors of the partition P (Eq. anchor-infill-partition, spacing delta)
+ * that flank the chunk's first latent.  With P_0 < P_1 < ... and
+ * m = floor(frames_per_chunk * i / delta), the frames {P_0, P_m, P_{m+1}}, an
+ * index past the last entry of P standing for the last entry (the boundary
+ * anchor L - 1), ascending and without repeats.  Writes 1 .. 3 frames to out3
+ * (host) and their number to *n_out.  i >= 0, frames_per_chunk >= 1,
+ * delta >= 1, L >= 1.  Host only. */
+ff_status ff_anchor_flank(int64_t i, int32_t frames_per_chunk, int32_t delta, int32_t L,
+                          int32_t* out3, int32_t* n_out);
 
 /* Euler step of the rectified-flow sampler (the Step of the wavefront
  * algorithm, App. Alg. 1 Phase B): x_out = x - dsigma * v elementwise over n

@@ -31,8 +31,9 @@ What it computes, following the paper (arxiv 2609.32540):
   distillation appendix): all chunks of one stage in one masked attention,
   used by the tests as an independent formulation.
 * Planner-side index sets: the anchor partition P (Eq. anchor-infill-
-  partition), the block/chunk counts, the window Gamma(i) (Sec. 3 notation)
-  and the forward-count model (Eq. forward-count).
+  partition), the block/chunk counts, the window Gamma(i) (Sec. 3 notation),
+  the long-horizon anchor set (the first anchor and the two entries of P that
+  flank a chunk) and the forward-count model (Eq. forward-count).
 
 Everything is float64 numpy; matrix products use numpy's matmul.
 """
@@ -204,6 +205,7 @@ class RendererCacheOracle:
     W: int
     history: Dict[Tuple[int, int], List[HistoryEntry]] = field(default_factory=dict)
     next_chunk: Dict[Tuple[int, int], int] = field(default_factory=dict)
+    n_published: Dict[Tuple[int, int], int] = field(default_factory=dict)
     anchors: Dict[int, Tuple[List[int], np.ndarray, np.ndarray]] = field(default_factory=dict)
 
     def _key(self, stage: int, layer: int) -> Tuple[int, int]:
@@ -228,15 +230,21 @@ class RendererCacheOracle:
         while len(lst) > self.W:
             lst.pop(0)
         self.next_chunk[key] = i + 1
+        self.n_published[key] = self.n_published.get(key, 0) + 1
 
     def ring_state(self, stage: int, layer: int) -> Tuple[List[int], int]:
-        """Slot table (slot c mod W holds chunk c, -1 when empty) and chunks published."""
+        """Slot table (slot c mod W holds chunk c, -1 when empty) and the number
+        of chunks published into the ring so far."""
         key = self._key(stage, layer)
         table = [-1] * self.W
         for e in self.history.get(key, []):
             table[e.chunk % self.W] = e.chunk
-        n = self.next_chunk.get(key)
-        return table, (0 if n is None else n)
+        return table, self.n_published.get(key, 0)
+
+    def expected_chunk(self, stage: int, layer: int) -> int:
+        """The chunk the ring expects next (-1 before the first publish)."""
+        n = self.next_chunk.get(self._key(stage, layer))
+        return -1 if n is None else n
 
     def history_concat(self, stage: int, layer: int) -> Tuple[np.ndarray, np.ndarray, List[int]]:
         lst = self.history.get(self._key(stage, layer), [])
@@ -427,6 +435,36 @@ def anchor_window(i: int, B_R: int, delta: int, L: int) -> List[int]:
     """Gamma(i) of Sec. 3 notation; indices past L-1 are replaced by L-1 (boundary side)."""
     u = (B_R * i) // (2 * delta)
     return sorted({min(v, L - 1) for v in (2 * u * delta, (2 * u + 1) * delta, (2 * u + 2) * delta)})
+
+
+def anchor_flank(i: int, B_R: int, delta: int, L: int) -> List[int]:
+    """Long-horizon anchor set of chunk i: the first anchor of P (Eq. anchor-
+    infill-partition, spacing delta) and the two entries of P that flank the
+    chunk's first latent B_R i, i.e. P_m and P_{m+1} with m = floor(B_R i / delta);
+    entries past the end of P are the last entry, the boundary anchor L-1."""
+    P = anchor_partition(L, delta)
+    m = (B_R * i) // delta
+
+    def at(j: int) -> int:
+        return P[min(j, len(P) - 1)]
+
+    return sorted({P[0], at(m), at(m + 1)})
+
+
+def anchor_frames(rule: str, i: int, B_R: int, L: int) -> List[int]:
+    """Anchor frames visible to chunk i under a workload's anchor rule:
+    "none"; "fixed:f0,f1,..." (the same frames for every chunk);
+    "gamma:<delta>" (Gamma(i) of Sec. 3 notation); "flank:<delta>" (anchor_flank)."""
+    if rule == "none":
+        return []
+    kind, _, arg = rule.partition(":")
+    if kind == "fixed":
+        return [int(v) for v in arg.split(",")]
+    if kind == "gamma":
+        return anchor_window(i, B_R, int(arg), L)
+    if kind == "flank":
+        return anchor_flank(i, B_R, int(arg), L)
+    raise ValueError(f"unknown anchor rule {rule!r}")
 
 
 def forward_counts(L: int, delta: int, B: int, S: int) -> Tuple[int, int, int]:

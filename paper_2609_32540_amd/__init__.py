@@ -3,4 +3,4 @@
 The compute path is the HIP library libff (paper_2609_32540_amd/csrc, C ABI in
 include/ff.h); `paper_2609_32540_amd.ff` is its Python binding.
 """
-from .ff import FFError, RendererCache, lib, rope_pair_split  # noqa: F401
+from .ff import FFError, RendererCache, lib  # noqa: F401

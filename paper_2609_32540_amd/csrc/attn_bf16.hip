@@ -229,11 +229,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     const int qi = min(q0 + 32 * cb + l32, nq - 1);
     const __bf16* qp = q + (int64_t(qi) * heads + head) * D + 8 * half;
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s) {
-      typedef float f32x8 __attribute__((ext_vector_type(8)));
-      const bf16x8 raw = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
-      qreg[cb][s] = raw;
-    }
+    for (int s = 0; s < C::KS; ++s) qreg[cb][s] = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
   }
 
   f32x16 o[kCB][C::DB];

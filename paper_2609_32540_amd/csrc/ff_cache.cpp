@@ -83,6 +83,20 @@ struct Layout {
 constexpr int kMaxTailSplit = 4;
 constexpr int kTailUnits = 256;
 
+// The descriptor as the cache uses it: all-zero rope pairs select the split of
+// the Wan2.1 backbone, d/2 - 2 floor(d/6) pairs on t and floor(d/6) on each of
+// h and w ((22, 21, 21) at d = 128, (12, 10, 10) at d = 64).
+ff_cache_desc resolve_desc(const ff_cache_desc& in) {
+  ff_cache_desc d = in;
+  if (d.rope_pairs_t == 0 && d.rope_pairs_h == 0 && d.rope_pairs_w == 0 && d.head_dim > 0) {
+    const int n_hw = d.head_dim / 6;
+    d.rope_pairs_t = d.head_dim / 2 - 2 * n_hw;
+    d.rope_pairs_h = n_hw;
+    d.rope_pairs_w = n_hw;
+  }
+  return d;
+}
+
 ff_status check_desc(const ff_cache_desc* d) {
   if (!d) return fail(FF_ERR_INVALID_ARG, "desc is NULL");
   if (d->num_stages < 1 || d->num_layers < 1)
@@ -145,6 +159,7 @@ struct ff_cache {
   // ring bookkeeping per (stage, layer): slot -> chunk (-1 empty), next chunk (-1 unset)
   std::vector<int64_t> slot_chunk;
   std::vector<int64_t> next_chunk;
+  std::vector<int64_t> n_published;   // publishes into the ring so far
   // anchor bookkeeping per layer
   std::vector<int32_t> anchor_frames;  // [layer][max_anchor_frames]
   std::vector<int32_t> anchor_count;
@@ -228,33 +243,41 @@ extern "C" {
 int32_t ff_abi_version(void) { return FF_ABI_VERSION; }
 
 size_t ff_cache_bytes(const ff_cache_desc* desc) {
-  if (check_desc(desc) != FF_OK) return 0;
+  if (!desc) {
+    fail(FF_ERR_INVALID_ARG, "desc is NULL");
+    return 0;
+  }
+  const ff_cache_desc d = resolve_desc(*desc);
+  if (check_desc(&d) != FF_OK) return 0;
   g_last_error.clear();
-  return make_layout(desc).total;
+  return make_layout(&d).total;
 }
 
 ff_status ff_cache_create(const ff_cache_desc* desc, void* dev_buf, size_t dev_bytes,
                           ff_cache** out) {
   return no_throw([&]() -> ff_status {
     if (!out) return fail(FF_ERR_INVALID_ARG, "out is NULL");
-    ff_status st = check_desc(desc);
+    if (!desc) return fail(FF_ERR_INVALID_ARG, "desc is NULL");
+    const ff_cache_desc rd = resolve_desc(*desc);
+    ff_status st = check_desc(&rd);
     if (st != FF_OK) return st;
     if (!dev_buf) return fail(FF_ERR_INVALID_ARG, "dev_buf is NULL");
     if (reinterpret_cast<uintptr_t>(dev_buf) % kAlign != 0)
       return fail(FF_ERR_BUFFER, "dev_buf must be %zu-byte aligned", kAlign);
-    const Layout L = make_layout(desc);
+    const Layout L = make_layout(&rd);
     if (dev_bytes < L.total)
       return fail(FF_ERR_BUFFER, "dev_bytes %zu < required %zu", dev_bytes, L.total);
     std::unique_ptr<ff_cache> c(new (std::nothrow) ff_cache);
     if (!c) return fail(FF_ERR_INVALID_ARG, "out of host memory");
-    c->desc = *desc;
+    c->desc = rd;
     c->layout = L;
     c->dev = static_cast<char*>(dev_buf);
-    const size_t rings = size_t(desc->num_stages) * desc->num_layers;
-    c->slot_chunk.assign(rings * desc->ring_chunks, -1);
+    const size_t rings = size_t(rd.num_stages) * rd.num_layers;
+    c->slot_chunk.assign(rings * rd.ring_chunks, -1);
     c->next_chunk.assign(rings, -1);
-    c->anchor_frames.assign(size_t(desc->num_layers) * (desc->max_anchor_frames + 1), 0);
-    c->anchor_count.assign(desc->num_layers, 0);
+    c->n_published.assign(rings, 0);
+    c->anchor_frames.assign(size_t(rd.num_layers) * (rd.max_anchor_frames + 1), 0);
+    c->anchor_count.assign(rd.num_layers, 0);
     *out = c.release();
     return ok();
   });
@@ -262,6 +285,12 @@ ff_status ff_cache_create(const ff_cache_desc* desc, void* dev_buf, size_t dev_b
 
 ff_status ff_cache_destroy(ff_cache* cache) {
   delete cache;
+  return ok();
+}
+
+ff_status ff_cache_get_desc(const ff_cache* cache, ff_cache_desc* out) {
+  if (!cache || !out) return fail(FF_ERR_INVALID_ARG, "cache and out must be non-NULL");
+  *out = cache->desc;
   return ok();
 }
 
@@ -316,6 +345,7 @@ ff_status ff_kv_publish(ff_cache* cache, int32_t stage, int32_t layer, int64_t c
   if (e != hipSuccess) return hip_status(e, "kv_publish launch");
   cache->slot_chunk[r * W + slot] = chunk_index;
   cache->next_chunk[r] = chunk_index + 1;
+  ++cache->n_published[r];
   return ok();
 }
 
@@ -444,10 +474,12 @@ ff_status check_scale(float softmax_scale) {
   return FF_OK;
 }
 
+// part / part_slots: where the tail-split partial results go (NULL: no split)
 ff_status chunk_attention_impl(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
                                const void* q, const void* k_cur, const void* v_cur, void* out,
                                float softmax_scale, const void* bank_k, const void* bank_v,
-                               int32_t n_frames, const int32_t* frame_index, void* stream) {
+                               int32_t n_frames, const int32_t* frame_index, float* part,
+                               int part_slots, void* stream) {
   ff::KvSegments segs;
   ff_status st = attention_read_set(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
                                     bank_k, bank_v, n_frames, frame_index, &segs);
@@ -462,7 +494,7 @@ ff_status chunk_attention_impl(ff_cache* cache, int32_t stage, int32_t layer, in
     const ff::TailSplit tail =
         choose_tail_split(ff::attention_bf16_units(chunk_tokens, heads),
                           ff::attention_bf16_key_tiles(segs), device_cus(),
-                          cache->layout.tail_slots, cache->tail_part(stage));
+                          part_slots, part);
     e = ff::launch_attention_bf16(q, out, chunk_tokens, heads, D, softmax_scale, segs, tail,
                                   static_cast<hipStream_t>(stream));
   }
@@ -478,8 +510,37 @@ ff_status ff_chunk_attention(ff_cache* cache, int32_t stage, int32_t layer, int6
                              const void* q, const void* k_cur, const void* v_cur, void* out,
                              float softmax_scale, void* stream) {
   return no_throw([&]() -> ff_status {
+    if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
+    const int s_ok = stage >= 0 && stage < cache->desc.num_stages;
     return chunk_attention_impl(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
-                                softmax_scale, nullptr, nullptr, 0, nullptr, stream);
+                                softmax_scale, nullptr, nullptr, 0, nullptr,
+                                s_ok ? cache->tail_part(stage) : nullptr,
+                                cache->layout.tail_slots, stream);
+  });
+}
+
+size_t ff_chunk_attention_workspace_bytes(const ff_cache* cache) {
+  if (!cache) {
+    fail(FF_ERR_INVALID_ARG, "cache is NULL");
+    return 0;
+  }
+  return cache->layout.tail_stage_bytes;
+}
+
+ff_status ff_chunk_attention_ws(ff_cache* cache, int32_t stage, int32_t layer, int64_t chunk_index,
+                                const void* q, const void* k_cur, const void* v_cur, void* out,
+                                float softmax_scale, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  return no_throw([&]() -> ff_status {
+    if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
+    if (workspace && check_aligned(workspace, "workspace") != FF_OK) return FF_ERR_INVALID_ARG;
+    int slots = 0;
+    if (workspace && cache->desc.dtype == FF_DT_BF16)
+      slots = int(std::min<size_t>(workspace_bytes / ff::attention_bf16_part_bytes(cache->desc.head_dim),
+                                   size_t(cache->layout.tail_slots)));
+    return chunk_attention_impl(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
+                                softmax_scale, nullptr, nullptr, 0, nullptr,
+                                slots > 0 ? static_cast<float*>(workspace) : nullptr, slots, stream);
   });
 }
 
@@ -489,9 +550,13 @@ ff_status ff_chunk_attention_bank(ff_cache* cache, int32_t stage, int32_t layer,
                                   const void* bank_k, const void* bank_v, int32_t n_frames,
                                   const int32_t* frame_index, void* stream) {
   return no_throw([&]() -> ff_status {
+    if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
     if (!bank_k) return fail(FF_ERR_INVALID_ARG, "bank_k must be non-NULL");
+    const int s_ok = stage >= 0 && stage < cache->desc.num_stages;
     return chunk_attention_impl(cache, stage, layer, chunk_index, q, k_cur, v_cur, out,
-                                softmax_scale, bank_k, bank_v, n_frames, frame_index, stream);
+                                softmax_scale, bank_k, bank_v, n_frames, frame_index,
+                                s_ok ? cache->tail_part(stage) : nullptr,
+                                cache->layout.tail_slots, stream);
   });
 }
 
@@ -529,7 +594,7 @@ ff_status ff_chunk_attention_batch(ff_cache* cache, int32_t n, const ff_attentio
 }
 
 ff_status ff_cache_ring_state(const ff_cache* cache, int32_t stage, int32_t layer,
-                              int64_t* slot_chunk, int64_t* published_count) {
+                              int64_t* slot_chunk, int64_t* next_chunk, int64_t* n_published) {
   if (!cache) return fail(FF_ERR_INVALID_ARG, "cache is NULL");
   ff_status st = check_stage_layer(cache, stage, layer);
   if (st != FF_OK) return st;
@@ -537,7 +602,8 @@ ff_status ff_cache_ring_state(const ff_cache* cache, int32_t stage, int32_t laye
   const int W = cache->desc.ring_chunks;
   if (slot_chunk)
     for (int s = 0; s < W; ++s) slot_chunk[s] = cache->slot_chunk[r * W + s];
-  if (published_count) *published_count = cache->next_chunk[r] < 0 ? 0 : cache->next_chunk[r];
+  if (next_chunk) *next_chunk = cache->next_chunk[r];
+  if (n_published) *n_published = cache->n_published[r];
   return ok();
 }
 
@@ -781,6 +847,26 @@ ff_status ff_anchor_window(int64_t i, int32_t frames_per_chunk, int32_t delta, i
     const int64_t f = std::min<int64_t>(m * delta, L - 1);
     if (n == 0 || out3[n - 1] != f) out3[n++] = int32_t(f);
   }
+  *n_out = n;
+  return ok();
+}
+
+ff_status ff_anchor_flank(int64_t i, int32_t frames_per_chunk, int32_t delta, int32_t L,
+                          int32_t* out3, int32_t* n_out) {
+  if (i < 0 || frames_per_chunk < 1 || delta < 1 || L < 1)
+    return fail(FF_ERR_INVALID_ARG, "need i >= 0, frames_per_chunk >= 1, delta >= 1, L >= 1");
+  if (!out3 || !n_out) return fail(FF_ERR_INVALID_ARG, "out3 / n_out is NULL");
+  // P_j = j delta on the grid, then L - 1 once past it; indices past |P| - 1 clamp
+  const int64_t n_grid = (L - 1) / delta + 1;
+  const int64_t last = n_grid - 1 + ((L - 1) % delta != 0 ? 1 : 0);
+  auto p = [&](int64_t j) -> int32_t {
+    j = std::min(j, last);
+    return j < n_grid ? int32_t(j * delta) : L - 1;
+  };
+  const int64_t m = int64_t(frames_per_chunk) * i / delta;
+  int n = 0;
+  for (int32_t f : {p(0), p(m), p(m + 1)})   // non-decreasing: p is monotone
+    if (n == 0 || out3[n - 1] != f) out3[n++] = f;
   *n_out = n;
   return ok();
 }

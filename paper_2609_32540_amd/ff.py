@@ -26,7 +26,7 @@ MAX_ANCHOR_FRAMES = 8
 MAX_ROPE_FRAMES = 16
 MAX_PACKED_CHUNKS = 128
 MAX_BATCH = 4
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 
 class FFError(RuntimeError):
@@ -82,15 +82,19 @@ SIGNATURES = [
     ("ff_cache_bytes", _SZ, [ctypes.POINTER(CacheDesc)]),
     ("ff_cache_create", _I32, [ctypes.POINTER(CacheDesc), _VP, _SZ, ctypes.POINTER(_VP)]),
     ("ff_cache_destroy", _I32, [_VP]),
+    ("ff_cache_get_desc", _I32, [_VP, ctypes.POINTER(CacheDesc)]),
     ("ff_rope3d", _I32, [_VP, _VP, _VP, _I32, _PI32, _VP]),
     ("ff_kv_publish", _I32, [_VP, _I32, _I32, _I64, _VP, _VP, _VP]),
     ("ff_anchor_set", _I32, [_VP, _I32, _I32, _PI32, _VP, _VP, _VP]),
     ("ff_chunk_attention", _I32, [_VP, _I32, _I32, _I64, _VP, _VP, _VP, _VP, ctypes.c_float, _VP]),
+    ("ff_chunk_attention_workspace_bytes", _SZ, [_VP]),
+    ("ff_chunk_attention_ws", _I32, [_VP, _I32, _I32, _I64, _VP, _VP, _VP, _VP, ctypes.c_float,
+                                     _VP, _SZ, _VP]),
     ("ff_chunk_attention_bank", _I32, [_VP, _I32, _I32, _I64, _VP, _VP, _VP, _VP, ctypes.c_float,
                                        _VP, _VP, _I32, _PI32, _VP]),
     ("ff_chunk_attention_batch", _I32, [_VP, _I32, ctypes.POINTER(AttentionItem), ctypes.c_float,
                                         _VP]),
-    ("ff_cache_ring_state", _I32, [_VP, _I32, _I32, _PI64, _PI64]),
+    ("ff_cache_ring_state", _I32, [_VP, _I32, _I32, _PI64, _PI64, _PI64]),
     ("ff_cache_anchor_state", _I32, [_VP, _I32, _PI32, _PI32]),
     ("ff_cache_read", _I32, [_VP, _I32, _I32, _I32, _VP, _VP, _VP]),
     ("ff_packed_attention", _I32, [ctypes.POINTER(PackedDesc), _VP, _VP, _VP, _VP, _VP, _VP,
@@ -101,6 +105,7 @@ SIGNATURES = [
                                        _SZ, _VP]),
     ("ff_anchor_partition", _I32, [_I32, _I32, _PI32, _I32, _PI32]),
     ("ff_anchor_window", _I32, [_I64, _I32, _I32, _I32, _PI32, _PI32]),
+    ("ff_anchor_flank", _I32, [_I64, _I32, _I32, _I32, _PI32, _PI32]),
     ("ff_euler_step", _I32, [_VP, _VP, _VP, _I64, ctypes.c_double, _I32, _VP]),
     ("ff_wavefront_run", _I32, [_I64, _I32, ctypes.POINTER(_VP), STAGE_FORWARD_FN, _VP, _PI64,
                                 _PI64]),
@@ -132,14 +137,29 @@ def _check(status: int) -> None:
         raise FFError(status, lib().ff_last_error().decode())
 
 
-def rope_pair_split(head_dim: int) -> Tuple[int, int, int]:
-    n_hw = head_dim // 6
-    return head_dim // 2 - 2 * n_hw, n_hw, n_hw
-
-
 def _stream_handle(device: torch.device, stream: Optional[torch.cuda.Stream]) -> int:
     s = stream if stream is not None else torch.cuda.current_stream(device)
     return s.cuda_stream
+
+
+def _empty_on(like: torch.Tensor, stream: Optional[torch.cuda.Stream],
+              device: Optional[torch.device] = None) -> torch.Tensor:
+    """A new tensor of like's shape and dtype (on `device`, default like's), allocated on
+    the stream the library writes it on: the caching allocator then keeps its memory from
+    being handed out again until that stream's work is done."""
+    dev = device if device is not None else like.device
+    if stream is None:
+        return torch.empty(like.shape, dtype=like.dtype, device=dev)
+    with torch.cuda.stream(stream):
+        return torch.empty(like.shape, dtype=like.dtype, device=dev)
+
+
+def _bytes_on(n: int, device: torch.device, stream: Optional[torch.cuda.Stream]) -> torch.Tensor:
+    """n device bytes allocated on the stream that uses them (see _empty_on)."""
+    if stream is None:
+        return torch.empty(n, dtype=torch.uint8, device=device)
+    with torch.cuda.stream(stream):
+        return torch.empty(n, dtype=torch.uint8, device=device)
 
 
 class RendererCache:
@@ -152,7 +172,7 @@ class RendererCache:
                  device: Optional[torch.device] = None):
         if dtype not in (torch.bfloat16, torch.float32):
             raise ValueError("dtype must be torch.bfloat16 or torch.float32")
-        rp = rope_pairs if rope_pairs is not None else rope_pair_split(head_dim)
+        rp = rope_pairs if rope_pairs is not None else (0, 0, 0)   # (0, 0, 0): the library's default
         self.desc = CacheDesc(stages, layers, ring_chunks, frames_per_chunk, grid_h, grid_w, heads,
                               head_dim, max_anchor_frames, rp[0], rp[1], rp[2], rope_theta,
                               FF_DT_BF16 if dtype == torch.bfloat16 else FF_DT_F32, 0)
@@ -171,6 +191,9 @@ class RendererCache:
         _check(L.ff_cache_create(ctypes.byref(self.desc), self.buffer.data_ptr(), self.nbytes,
                                  ctypes.byref(h)))
         self._h = h
+        resolved = CacheDesc()
+        _check(L.ff_cache_get_desc(h, ctypes.byref(resolved)))
+        self.rope_pairs = (resolved.rope_pairs_t, resolved.rope_pairs_h, resolved.rope_pairs_w)
 
     # ------------------------------------------------------------------
     def close(self) -> None:
@@ -233,12 +256,40 @@ class RendererCache:
         kp = self._tensor(k, self.chunk_tokens, "k")
         vp = self._tensor(v, self.chunk_tokens, "v")
         if out is None:
-            out = torch.empty_like(q)
+            out = _empty_on(q, stream)
         op = self._tensor(out, self.chunk_tokens, "out")
         if scale is None:
             scale = 1.0 / math.sqrt(self.head_dim)
         _check(lib().ff_chunk_attention(self._h, stage, layer, chunk, qp, kp, vp, op,
                                         ctypes.c_float(scale), _stream_handle(self.device, stream)))
+        return out
+
+    def workspace_bytes(self) -> int:
+        """ff_chunk_attention_workspace_bytes: workspace of one ff_chunk_attention_ws call."""
+        return lib().ff_chunk_attention_workspace_bytes(self._h)
+
+    def chunk_attention_ws(self, stage: int, layer: int, chunk: int, q: torch.Tensor,
+                           k: torch.Tensor, v: torch.Tensor, workspace: Optional[torch.Tensor],
+                           out: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+                           stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        """ff_chunk_attention_ws: the tail-split partials go to `workspace` (a uint8 device
+        tensor, or None for an unsplit launch) instead of the cache's per-stage scratch."""
+        qp = self._tensor(q, self.chunk_tokens, "q")
+        kp = self._tensor(k, self.chunk_tokens, "k")
+        vp = self._tensor(v, self.chunk_tokens, "v")
+        if out is None:
+            out = _empty_on(q, stream)
+        op = self._tensor(out, self.chunk_tokens, "out")
+        wp, wn = None, 0
+        if workspace is not None:
+            if workspace.device != self.device or not workspace.is_contiguous():
+                raise ValueError("workspace must be a contiguous tensor on the cache's device")
+            wp, wn = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+        if scale is None:
+            scale = 1.0 / math.sqrt(self.head_dim)
+        _check(lib().ff_chunk_attention_ws(self._h, stage, layer, chunk, qp, kp, vp, op,
+                                           ctypes.c_float(scale), wp, wn,
+                                           _stream_handle(self.device, stream)))
         return out
 
     def chunk_attention_bank(self, stage: int, layer: int, chunk: int, q: torch.Tensor,
@@ -252,7 +303,7 @@ class RendererCache:
         kp = self._tensor(k, self.chunk_tokens, "k")
         vp = self._tensor(v, self.chunk_tokens, "v")
         if out is None:
-            out = torch.empty_like(q)
+            out = _empty_on(q, stream)
         op = self._tensor(out, self.chunk_tokens, "out")
         if bank_k.shape[0] % self.tokens_per_frame:
             raise ValueError("the bank must hold whole frames")
@@ -286,7 +337,7 @@ class RendererCache:
             a.v_cur = self._tensor(it["v"], self.chunk_tokens, "v")
             out = it.get("out")
             if out is None:
-                out = torch.empty_like(it["q"])
+                out = _empty_on(it["q"], stream)
             a.out = self._tensor(out, self.chunk_tokens, "out")
             outs.append(out)
             if it.get("bank_k") is not None:
@@ -310,10 +361,17 @@ class RendererCache:
 
     # ------------------------------------------------------------------
     def ring_state(self, stage: int, layer: int) -> Tuple[List[int], int]:
+        """(slot table, number of chunks published into the ring so far)."""
         slots = (ctypes.c_int64 * self.ring_chunks)()
         count = ctypes.c_int64()
-        _check(lib().ff_cache_ring_state(self._h, stage, layer, slots, ctypes.byref(count)))
+        _check(lib().ff_cache_ring_state(self._h, stage, layer, slots, None, ctypes.byref(count)))
         return list(slots), count.value
+
+    def next_chunk(self, stage: int, layer: int) -> int:
+        """The chunk the ring expects next (-1 before its first publish)."""
+        nxt = ctypes.c_int64()
+        _check(lib().ff_cache_ring_state(self._h, stage, layer, None, ctypes.byref(nxt), None))
+        return nxt.value
 
     def anchor_state(self, layer: int) -> List[int]:
         n = ctypes.c_int32()
@@ -328,8 +386,9 @@ class RendererCache:
             n_tok = len(self.anchor_state(layer)) * self.tokens_per_frame
         else:
             n_tok = self.chunk_tokens
-        k = torch.empty((n_tok, self.heads, self.head_dim), dtype=self.dtype, device=self.device)
-        v = torch.empty_like(k)
+        shape = torch.empty((n_tok, self.heads, self.head_dim), dtype=self.dtype, device="meta")
+        k = _empty_on(shape, stream, self.device)
+        v = _empty_on(shape, stream, self.device)
         if n_tok:
             _check(lib().ff_cache_read(self._h, stage, layer, slot, k.data_ptr(), v.data_ptr(),
                                        _stream_handle(self.device, stream)))
@@ -401,7 +460,7 @@ def packed_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, *, n_chu
     kp = _dense(k, shape, dt, dev, "k")
     vp = _dense(v, shape, dt, dev, "v")
     if out is None:
-        out = torch.empty_like(q)
+        out = _empty_on(q, stream)
     op = _dense(out, shape, dt, dev, "out")
     lp = _dense(lse, shape[:2], torch.float32, dev, "lse") if lse is not None else None
     if scale is None:
@@ -422,11 +481,11 @@ def packed_attention_bwd(q, k, v, out, dout, lse, *, n_chunks: int, window: int,
     ptrs = [_dense(t, shape, dt, dev, n) for t, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out"),
                                                       (dout, "dout"))]
     lp = _dense(lse, shape[:2], torch.float32, dev, "lse")
-    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
-    dak = torch.empty_like(anchor_k) if anchor_k is not None else None
-    dav = torch.empty_like(anchor_v) if anchor_v is not None else None
+    dq, dk, dv = _empty_on(q, stream), _empty_on(k, stream), _empty_on(v, stream)
+    dak = _empty_on(anchor_k, stream) if anchor_k is not None else None
+    dav = _empty_on(anchor_v, stream) if anchor_v is not None else None
     ws_bytes = lib().ff_packed_attention_bwd_workspace(ctypes.byref(desc))
-    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
+    ws = _bytes_on(max(ws_bytes, 16), dev, stream)
     if scale is None:
         scale = 1.0 / math.sqrt(shape[2])
     _check(lib().ff_packed_attention_bwd(
@@ -456,6 +515,30 @@ def anchor_window(i: int, frames_per_chunk: int, delta: int, L: int) -> List[int
     return list(out)[: n.value]
 
 
+def anchor_flank(i: int, frames_per_chunk: int, delta: int, L: int) -> List[int]:
+    """ff_anchor_flank: {P_0, P_m, P_m+1}, the first anchor and the two flanking chunk i."""
+    out = (ctypes.c_int32 * 3)()
+    n = ctypes.c_int32()
+    _check(lib().ff_anchor_flank(i, frames_per_chunk, delta, L, out, ctypes.byref(n)))
+    return list(out)[: n.value]
+
+
+def anchor_frames(rule: str, i: int, frames_per_chunk: int, L: int) -> List[int]:
+    """Anchor frames chunk i reads under a named rule, from the library's index
+    sets: "none", "fixed:f0,f1,...", "gamma:<delta>" (ff_anchor_window) or
+    "flank:<delta>" (ff_anchor_flank)."""
+    if rule == "none":
+        return []
+    kind, _, arg = rule.partition(":")
+    if kind == "fixed":
+        return [int(v) for v in arg.split(",")]
+    if kind == "gamma":
+        return anchor_window(i, frames_per_chunk, int(arg), L)
+    if kind == "flank":
+        return anchor_flank(i, frames_per_chunk, int(arg), L)
+    raise FFError(f"unknown anchor rule {rule!r}")
+
+
 def euler_step(x: torch.Tensor, v: torch.Tensor, dsigma: float, out: Optional[torch.Tensor] = None,
                stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """ff_euler_step: out = x - dsigma * v (out may be x)."""
@@ -464,7 +547,7 @@ def euler_step(x: torch.Tensor, v: torch.Tensor, dsigma: float, out: Optional[to
     if x.shape != v.shape or not x.is_contiguous() or not v.is_contiguous():
         raise ValueError("x and v must be contiguous tensors of one shape")
     if out is None:
-        out = torch.empty_like(x)
+        out = _empty_on(x, stream)
     if out.shape != x.shape or out.dtype != x.dtype or not out.is_contiguous():
         raise ValueError("out must match x")
     _check(lib().ff_euler_step(x.data_ptr(), v.data_ptr(), out.data_ptr(), x.numel(),

@@ -56,7 +56,11 @@ class Workload:
     layers: int
     n_chunks: int                 # chunks generated in sequence
     input_scale: float
-    anchor_rule: str              # "none" | "fixed:<f0>,<f1>,..." | "window" | "every8"
+    # which anchor frames each chunk reads, by name only (the rule itself is
+    # the method's, not this module's): "none", "fixed:<f0>,<f1>,...",
+    # "gamma:<delta>" (the window Gamma(i)) or "flank:<delta>" (the first
+    # anchor and the two partition entries flanking the chunk)
+    anchor_rule: str
     max_anchor_frames: int
 
     @property
@@ -79,42 +83,6 @@ class Workload:
     def latent_frames(self) -> int:
         return self.n_chunks * self.frames_per_chunk
 
-    def anchor_frames_for_chunk(self, i: int) -> List[int]:
-        """Latent frame positions of the anchor segment visible to chunk i."""
-        rule = self.anchor_rule
-        if rule == "none":
-            return []
-        if rule.startswith("fixed:"):
-            return [int(v) for v in rule[len("fixed:"):].split(",")]
-        if rule == "window":
-            # Sec. 3 notation: Gamma(i) = {2u D, (2u+1) D, (2u+2) D},
-            # u = floor(B_R i / (2 D)), D = 10; indices past the last latent are
-            # replaced by the last latent and de-duplicated.
-            delta = 10
-            last = max(self.latent_frames - 1, 0)
-            u = (self.frames_per_chunk * i) // (2 * delta)
-            fr = [min(v, last) for v in (2 * u * delta, (2 * u + 1) * delta, (2 * u + 2) * delta)]
-            return sorted(set(fr))
-        if rule == "every8":
-            # one 1-frame anchor every 8 chunks (every 24 latents), plus the end
-            # latent; chunk i reads the first-frame anchor and its two flanking
-            # anchors.
-            period = 8 * self.frames_per_chunk
-            last = self.latent_frames - 1
-            m = i // 8
-            return sorted({0, min(period * m, last), min(period * (m + 1), last)})
-        raise ValueError(rule)
-
-    def anchor_update_chunks(self) -> List[int]:
-        """Chunks before which the anchor segment changes."""
-        out, prev = [], None
-        for i in range(self.n_chunks):
-            fr = self.anchor_frames_for_chunk(i)
-            if fr != prev:
-                out.append(i)
-                prev = fr
-        return out
-
 
 WORKLOADS: Dict[str, Workload] = {
     # tiny CPU-checkable case
@@ -122,16 +90,16 @@ WORKLOADS: Dict[str, Workload] = {
                          "fixed:0,15", 2),
     # 1.3B-shaped, 480p
     "1.3b-480p": Workload("1.3b-480p", 2, "bf16", 12, 128, 30, 52, 3, 4, 4, 30, 27,
-                          1.0 / math.sqrt(128.0), "window", 3),
+                          1.0 / math.sqrt(128.0), "gamma:10", 3),
     # 1.3B-shaped, 480p, long horizon (87 chunks = 261 latent frames)
     "1.3b-480p-long": Workload("1.3b-480p-long", 3, "bf16", 12, 128, 30, 52, 3, 4, 4, 30, 87,
-                               1.0 / math.sqrt(128.0), "every8", 3),
+                               1.0 / math.sqrt(128.0), "flank:24", 3),
     # 14B-shaped, 480p
     "14b-480p": Workload("14b-480p", 4, "bf16", 40, 128, 30, 52, 3, 4, 4, 40, 27, 1.0,
-                         "window", 3),
+                         "gamma:10", 3),
     # 14B-shaped, 720p
     "14b-720p": Workload("14b-720p", 5, "bf16", 40, 128, 45, 80, 3, 4, 4, 40, 27, 1.0,
-                         "window", 3),
+                         "gamma:10", 3),
 }
 
 

@@ -18,6 +18,11 @@ F32_MAX_ABS = 1e-5
 F32_REL_L2 = 1e-5
 
 
+def anchor_frames(w: "synth.Workload", i: int) -> List[int]:
+    """Anchor frames chunk i of workload w reads, by the oracle's reading of its rule."""
+    return fo.anchor_frames(w.anchor_rule, i, w.frames_per_chunk, w.latent_frames)
+
+
 def device() -> torch.device:
     return torch.device("cuda", 0)
 
@@ -116,7 +121,7 @@ class PairedRun:
              scale: Optional[float] = None) -> Optional[torch.Tensor]:
         """RoPE, attention, publish of one (chunk, stage, layer) on both sides."""
         w = self.w
-        frames_a = w.anchor_frames_for_chunk(chunk)
+        frames_a = anchor_frames(w, chunk)
         if self.anchor_frames.get(layer) != frames_a:
             self.set_anchors(layer, frames_a)
         q = synth.chunk_tensor(w, synth.T_Q, chunk, stage, layer)
@@ -126,7 +131,9 @@ class PairedRun:
         frames = fo.chunk_frames(chunk, w.frames_per_chunk)
         if self.rope:
             self.cache.rope3d(qd, kd, frames)
-            q_ref, k_ref = oracle_rope(w, q, frames), oracle_rope(w, k, frames)
+            # the oracle rotates Q only for a checked step (K always: it is published)
+            q_ref = oracle_rope(w, q, frames) if check else None
+            k_ref = oracle_rope(w, k, frames)
         else:
             q_ref, k_ref = exact(q), exact(k)
         v_ref = exact(v)

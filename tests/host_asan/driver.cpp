@@ -61,6 +61,8 @@ static void ring_sequences() {
       FakeDevice dev(n);
       ff_cache* h = nullptr;
       EXPECT(ff_cache_create(&d, dev.ptr(), n, &h) == FF_OK && h);
+      ff_cache_desc used = {};
+      EXPECT(ff_cache_get_desc(h, &used) == FF_OK && used.ring_chunks == W);
       FakeDevice chunk(2 * 198 * 3 * 128 * 4 + 1024);
       char* t = static_cast<char*>(chunk.ptr());
       std::vector<int32_t> ft(8);
@@ -74,6 +76,14 @@ static void ring_sequences() {
         for (int s = 0; s < 2; ++s)
           for (int l = 0; l < 2; ++l) {
             EXPECT(ff_chunk_attention(h, s, l, c, t, t, t, t, 0.125f, nullptr) == FF_OK);
+            // a caller workspace: the stage's full size, a smaller one, none
+            const size_t ws = ff_chunk_attention_workspace_bytes(h);
+            EXPECT(ff_chunk_attention_ws(h, s, l, c, t, t, t, t, 0.125f, dev.ptr(), ws, nullptr) ==
+                   FF_OK);
+            EXPECT(ff_chunk_attention_ws(h, s, l, c, t, t, t, t, 0.125f, dev.ptr(), ws / 3,
+                                         nullptr) == FF_OK);
+            EXPECT(ff_chunk_attention_ws(h, s, l, c, t, t, t, t, 0.125f, nullptr, 0, nullptr) ==
+                   FF_OK);
             // the bank path: out-of-order frames, runs of consecutive frames, a duplicate
             const int32_t frames[5] = {7, 2, 3, 0, 1};
             EXPECT(ff_chunk_attention_bank(h, s, l, c, t, t, t, t, 0.125f, t, t, 5, frames,
@@ -105,8 +115,9 @@ static void ring_sequences() {
               EXPECT(ff_chunk_attention_batch(h, 3, items, 0.125f, nullptr) == FF_ERR_ORDER);
             EXPECT(ff_kv_publish(h, s, l, c, t, t, nullptr) == FF_OK);
             std::vector<int64_t> slots(W, -2);
-            int64_t count = -1;
-            EXPECT(ff_cache_ring_state(h, s, l, slots.data(), &count) == FF_OK && count == c + 1);
+            int64_t next = -1, count = -1;   // first publish was chunk 5
+            EXPECT(ff_cache_ring_state(h, s, l, slots.data(), &next, &count) == FF_OK &&
+                   next == c + 1 && count == c - 4);
             for (int slot = 0; slot < W; ++slot) {   // Tail_W of chunks 5 .. c
               int64_t want = -1;
               for (int64_t x = c; x >= 5 && x > c - W; --x)
@@ -191,6 +202,8 @@ static void planner_euler_wavefront() {
   EXPECT(ff_anchor_partition(261, 10, out.data(), 2, &n) == FF_ERR_BUFFER && n == 27);
   int32_t w3[3];
   EXPECT(ff_anchor_window(2, 3, 10, 81, w3, &n) == FF_OK && n == 3 && w3[0] == 0 && w3[2] == 20);
+  EXPECT(ff_anchor_flank(86, 3, 24, 261, w3, &n) == FF_OK && n == 3 && w3[1] == 240 && w3[2] == 260);
+  EXPECT(ff_anchor_flank(0, 3, 24, 261, w3, &n) == FF_OK && n == 2 && w3[1] == 24);
   FakeDevice buf(1 << 16);
   char* t = static_cast<char*>(buf.ptr());
   EXPECT(ff_euler_step(t, t + 8192, t, 64, 0.25, FF_DT_BF16, nullptr) == FF_OK);

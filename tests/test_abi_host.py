@@ -34,11 +34,11 @@ def desc(**kw):
 def test_library_exports_every_header_symbol():
     L = ff.lib()
     names = header_functions()
-    assert len(names) == 22
+    assert len(names) == 26
     for n in names:
         assert hasattr(L, n), n
     assert {n for n, _, _ in ff.SIGNATURES} == set(names)
-    assert L.ff_abi_version() == ff.ABI_VERSION == 3
+    assert L.ff_abi_version() == ff.ABI_VERSION == 4
 
 
 def test_cache_bytes_layout():
@@ -97,11 +97,11 @@ def test_create_checks_buffer():
 def test_fresh_cache_state_and_host_validation():
     L, h, _ = make_handle()
     slots = (ctypes.c_int64 * 4)()
-    cnt = ctypes.c_int64(-5)
-    assert L.ff_cache_ring_state(h, 3, 1, slots, ctypes.byref(cnt)) == 0
-    assert list(slots) == [-1] * 4 and cnt.value == 0
-    assert L.ff_cache_ring_state(h, 4, 0, slots, ctypes.byref(cnt)) == 4   # stage range
-    assert L.ff_cache_ring_state(h, 0, 2, slots, ctypes.byref(cnt)) == 4   # layer range
+    cnt, nxt = ctypes.c_int64(-5), ctypes.c_int64(-5)
+    assert L.ff_cache_ring_state(h, 3, 1, slots, ctypes.byref(nxt), ctypes.byref(cnt)) == 0
+    assert list(slots) == [-1] * 4 and cnt.value == 0 and nxt.value == -1
+    assert L.ff_cache_ring_state(h, 4, 0, slots, None, ctypes.byref(cnt)) == 4   # stage range
+    assert L.ff_cache_ring_state(h, 0, 2, slots, None, ctypes.byref(cnt)) == 4   # layer range
     nfr = ctypes.c_int32(-1)
     assert L.ff_cache_anchor_state(h, 0, ctypes.byref(nfr), None) == 0 and nfr.value == 0
     dummy = FAKE_DEV
@@ -128,8 +128,14 @@ def test_fresh_cache_state_and_host_validation():
     # anchor_set with 0 frames clears without launching anything
     assert L.ff_anchor_set(h, 1, 0, None, None, None, None) == 0
     # state unchanged by the failed calls
-    assert L.ff_cache_ring_state(h, 0, 0, slots, ctypes.byref(cnt)) == 0
-    assert list(slots) == [-1] * 4 and cnt.value == 0
+    assert L.ff_cache_ring_state(h, 0, 0, slots, ctypes.byref(nxt), ctypes.byref(cnt)) == 0
+    assert list(slots) == [-1] * 4 and cnt.value == 0 and nxt.value == -1
+    # the workspace variant validates like ff_chunk_attention; its size is one stage's partials
+    assert L.ff_chunk_attention_ws(h, 0, 5, 0, dummy, dummy, dummy, dummy, 0.1, None, 0, None) == 4
+    assert L.ff_chunk_attention_ws(h, 0, 0, 0, dummy, dummy, dummy, dummy, 0.1, dummy + 4, 64,
+                                   None) == 1
+    assert L.ff_chunk_attention_workspace_bytes(h) == 4 * 228 * (256 * 128 + 2 * 256) * 4
+    assert L.ff_chunk_attention_workspace_bytes(None) == 0
     assert L.ff_cache_destroy(h) == 0
     assert L.ff_cache_destroy(None) == 0
 
@@ -221,6 +227,32 @@ def test_anchor_window_matches_oracle():
     assert ff.lib().ff_anchor_window(-1, 3, 10, 261, out, ctypes.byref(n)) == 1
 
 
+def test_anchor_flank_matches_oracle():
+    from oracle import ff_oracle as fo
+    for L in (1, 2, 18, 21, 81, 261):
+        for B_R in (1, 3, 4):
+            for delta in (1, 5, 10, 24):
+                for i in range(0, -(-L // B_R) + 3):
+                    assert ff.anchor_flank(i, B_R, delta, L) == fo.anchor_flank(i, B_R, delta, L), \
+                        (L, B_R, delta, i)
+    out = (ctypes.c_int32 * 3)()
+    n = ctypes.c_int32()
+    assert ff.lib().ff_anchor_flank(-1, 3, 24, 261, out, ctypes.byref(n)) == 1
+    assert ff.lib().ff_anchor_flank(0, 3, 0, 261, out, ctypes.byref(n)) == 1
+    assert ff.lib().ff_anchor_flank(0, 3, 24, 261, None, ctypes.byref(n)) == 1
+
+
+def test_workload_anchor_rules_library_equals_oracle():
+    # the benchmark takes each chunk's anchor frames from the library, the GPU
+    # tests from the oracle: both readings agree on every chunk of every workload
+    import synth
+    from oracle import ff_oracle as fo
+    for w in synth.WORKLOADS.values():
+        for i in range(w.n_chunks):
+            assert ff.anchor_frames(w.anchor_rule, i, w.frames_per_chunk, w.latent_frames) == \
+                fo.anchor_frames(w.anchor_rule, i, w.frames_per_chunk, w.latent_frames), (w.name, i)
+
+
 def test_euler_and_wavefront_host_validation():
     L = ff.lib()
     assert L.ff_euler_step(FAKE_DEV, FAKE_DEV + 4096, FAKE_DEV, -1, 0.5, 0, None) == 1
@@ -237,3 +269,25 @@ def test_euler_and_wavefront_host_validation():
     assert L.ff_wavefront_run(0, 2, arr, fn, None, ctypes.byref(r), ctypes.byref(f)) == 1
     assert L.ff_wavefront_run(3, 0, arr, fn, None, ctypes.byref(r), ctypes.byref(f)) == 1
     assert not calls
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_rope_split_default_lives_in_the_library(head_dim):
+    # all-zero rope pairs select the backbone's split inside the library; it equals
+    # the oracle's reading of the paper's (22, 21, 21) split for every head size
+    from oracle import ff_oracle as fo
+    L, h, _ = make_handle(head_dim=head_dim, rope_pairs_t=0, rope_pairs_h=0, rope_pairs_w=0)
+    got = ff.CacheDesc()
+    assert L.ff_cache_get_desc(h, ctypes.byref(got)) == 0
+    assert (got.rope_pairs_t, got.rope_pairs_h, got.rope_pairs_w) == fo.rope_pair_split(head_dim)
+    assert got.head_dim == head_dim and got.num_heads == 12
+    assert L.ff_cache_destroy(h) == 0
+    # an explicit split is kept as given, and a wrong sum is still rejected
+    L, h, _ = make_handle(head_dim=head_dim, rope_pairs_t=head_dim // 2, rope_pairs_h=0,
+                          rope_pairs_w=0)
+    assert L.ff_cache_get_desc(h, ctypes.byref(got)) == 0
+    assert (got.rope_pairs_t, got.rope_pairs_h, got.rope_pairs_w) == (head_dim // 2, 0, 0)
+    assert L.ff_cache_destroy(h) == 0
+    bad = desc(head_dim=head_dim, rope_pairs_t=1, rope_pairs_h=0, rope_pairs_w=0)
+    assert L.ff_cache_bytes(ctypes.byref(bad)) == 0
+    assert L.ff_cache_get_desc(None, ctypes.byref(got)) == 1

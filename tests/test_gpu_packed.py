@@ -13,7 +13,7 @@ import synth
 from oracle import ff_oracle as fo
 from paper_2609_32540_amd import ff
 
-from gpu_util import check_attention, exact, make_cache, to_dev
+from gpu_util import anchor_frames, check_attention, exact, make_cache, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -137,22 +137,26 @@ def test_packed_equals_sequential_ring(dtype, d):
         assert np.abs(gp - gs).max() <= 1e-5
 
 
-def test_packed_full_size_sampled_rows():
-    """1.3B 480p clip (27 chunks x 4680 tokens, 12 heads x 128, W = 4, anchor
-    windows Gamma(i)): one launch, checked on sampled rows of chunks at the
-    start, the middle and the end against the float64 oracle over the visible
-    keys; inputs seeded N(0,1) drawn on the device."""
-    w = synth.WORKLOADS["1.3b-480p"]
+@pytest.mark.parametrize("name", ["1.3b-480p", "14b-720p"])
+def test_packed_full_size_sampled_rows(name):
+    """A whole clip of one stage (27 chunks, W = 4, anchor windows Gamma(i)) at
+    the 1.3B 480p shape (4680-token chunks, 12 heads) and at the 14B 720p shape
+    the benchmark times (10800-token chunks, 40 heads): one launch, checked on
+    sampled rows (incl. the ragged last query tile) of chunks at the start, the
+    middle and the end against the float64 oracle over the visible keys (the
+    renderer rows of the packed mask M, Alg. 2); inputs seeded N(0,1) drawn on
+    the device."""
+    w = synth.WORKLOADS[name]
     n, W, Nq, G = w.n_chunks, w.ring_chunks, w.chunk_tokens, w.tokens_per_frame
     dev = torch.device("cuda", 0)
     g = torch.Generator(device=dev)
     g.manual_seed(1234)
     shape = (n * Nq, w.heads, w.head_dim)
     q, k, v = (torch.randn(shape, generator=g, device=dev).to(torch.bfloat16) for _ in range(3))
-    frames = sorted({f for c in range(n) for f in w.anchor_frames_for_chunk(c)})
+    frames = sorted({f for c in range(n) for f in anchor_frames(w, c)})
     a_shape = (len(frames) * G, w.heads, w.head_dim)
     ak, av = (torch.randn(a_shape, generator=g, device=dev).to(torch.bfloat16) for _ in range(2))
-    table = [[frames.index(f) for f in w.anchor_frames_for_chunk(c)] for c in range(n)]
+    table = [[frames.index(f) for f in anchor_frames(w, c)] for c in range(n)]
     scale = 1.0 / math.sqrt(w.head_dim)
     out = ff.packed_attention(q, k, v, n_chunks=n, window=W, anchor_k=ak, anchor_v=av,
                               frame_tokens=G, anchors_of_chunk=table, scale=scale)

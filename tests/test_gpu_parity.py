@@ -108,7 +108,9 @@ def test_order_errors_leave_state_unchanged():
         cache.kv_publish(0, 0, 4, k[:-1], k[:-1])
     assert cache.ring_state(0, 0) == before
     cache.kv_publish(0, 0, 4, k, k)
-    assert cache.ring_state(0, 0) == ([4, 3], 5)
+    # two chunks published (the first at chunk 3), chunk 5 expected next
+    assert cache.ring_state(0, 0) == ([4, 3], 2)
+    assert cache.next_chunk(0, 0) == 5
 
 
 # --------------------------------------------------------------------------
@@ -380,15 +382,36 @@ def test_long_horizon_schedule():
     assert run.cache.ring_state(0, 0) == ([84, 85, 86, 83], 87)
 
 
+def test_long_horizon_full_grid_sampled_rows():
+    # the long-horizon workload at its own shape (30x52 grid, 12 heads, d 128,
+    # W = 4, inputs N(0,1)/sqrt(128)) through RoPE, attention and publish for
+    # chunks 0 .. 10: the ring wraps from chunk 4 on and the anchor window moves
+    # at chunk 8 ({0, 24} -> {0, 24, 48}); sampled rows of chunks 6 .. 10
+    w = synth.WORKLOADS["1.3b-480p-long"]
+    run = PairedRun(w, stages=1, layers=1)
+    nq = w.chunk_tokens
+    rows = np.concatenate([np.arange(0, 384), np.arange(nq - 384, nq)])
+    heads = [0, w.heads - 1]
+    for c in range(11):
+        run.step(c, 0, 0, check=c >= 6, rows=rows, heads=heads)
+        if c == 7:
+            assert run.cache.anchor_state(0) == [0, 24]
+    assert run.cache.anchor_state(0) == [0, 24, 48]
+    assert run.cache.ring_state(0, 0) == ([8, 9, 10, 7], 11)
+    assert len(run.results) == 5
+
+
 # --------------------------------------------------------------------------
 # full-size workloads: one steady-state chunk-stage, sampled rows
 # --------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name", ["1.3b-480p", "14b-480p", "14b-720p"])
-def test_full_size_sampled_rows(name):
+@pytest.mark.parametrize("name,rope", [("1.3b-480p", False), ("14b-480p", False), ("14b-720p", True)])
+def test_full_size_sampled_rows(name, rope):
+    # 14B 720p (the benchmarked chunk-stage) runs the whole step: RoPE of Q and K
+    # (and of the anchor K), attention over [anchors | ring | chunk], publish
     w = synth.WORKLOADS[name]
     stage, layer, chunk = 1, 3, w.ring_chunks + 3          # ring full, steady state
-    run = PairedRun(w, stages=stage + 1, layers=layer + 1, rope=False)
+    run = PairedRun(w, stages=stage + 1, layers=layer + 1, rope=rope)
     nq = w.chunk_tokens
     rows = np.concatenate([np.arange(0, 512), np.arange(nq - 512, nq)])   # includes the ragged tail tile
     heads = [0, w.heads - 1]
@@ -396,7 +419,8 @@ def test_full_size_sampled_rows(name):
         run.step(c, stage, layer, check=(c == chunk), rows=rows, heads=heads)
     # the ring holds the previous W chunks plus this one; check one full slot bit for bit
     table, count = run.cache.ring_state(stage, layer)
-    assert count == chunk + 1 and sorted(table) == list(range(chunk - w.ring_chunks + 1, chunk + 1))
+    assert count == w.ring_chunks + 1 and run.cache.next_chunk(stage, layer) == chunk + 1
+    assert sorted(table) == list(range(chunk - w.ring_chunks + 1, chunk + 1))
     entries = {e.chunk: e for e in run.oracle.history[(stage, layer)]}
     kg, vg = run.cache.read(stage, layer, chunk % w.ring_chunks)
     np.testing.assert_array_equal(exact(kg), entries[chunk].K)

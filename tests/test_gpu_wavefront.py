@@ -11,7 +11,7 @@ import synth
 from oracle import ff_oracle as fo
 from paper_2609_32540_amd import ff
 
-from gpu_util import exact, make_cache, to_dev
+from gpu_util import anchor_frames, exact, make_cache, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -65,7 +65,7 @@ def make_stub(cache, w, X, layers, bank=None):
                     h = cache.chunk_attention(s, l, i, q, k, v, stream=stream)
                 else:
                     bk, bv, bframes = bank[l]
-                    idx = [bframes.index(f) for f in w.anchor_frames_for_chunk(i)]
+                    idx = [bframes.index(f) for f in anchor_frames(w, i)]
                     h = cache.chunk_attention_bank(s, l, i, q, k, v, bk, bv, idx, stream=stream)
                 cache.kv_publish(s, l, i, k, v, stream=stream)
             k_idx = S - s
@@ -141,9 +141,9 @@ def test_wavefront_with_anchor_windows_from_a_bank():
     N_R = 27
     w = synth.small_workload("wave-bank", dtype="bf16", heads=2, head_dim=128, grid_h=4,
                              grid_w=7, ring_chunks=4, stages=S, layers=1, n_chunks=N_R,
-                             anchor_rule="window", max_anchor_frames=3)
-    frames = sorted({f for i in range(N_R) for f in w.anchor_frames_for_chunk(i)})
-    assert len({tuple(w.anchor_frames_for_chunk(i)) for i in range(N_R)}) > 2
+                             anchor_rule="gamma:10", max_anchor_frames=3)
+    frames = sorted({f for i in range(N_R) for f in anchor_frames(w, i)})
+    assert len({tuple(anchor_frames(w, i)) for i in range(N_R)}) > 2
     ak, av = synth.anchor_tensors(w, frames, 0)
     akd, avd = to_dev(ak), to_dev(av)
     G = w.tokens_per_frame
@@ -179,7 +179,7 @@ def test_wavefront_with_anchor_windows_from_a_bank():
     cur = None
     for i in range(N_R):
         q, k, v = (to_dev(synth.chunk_tensor(w, t, i, 0, 0)) for t in (synth.T_Q, synth.T_K, synth.T_V))
-        win = w.anchor_frames_for_chunk(i)
+        win = anchor_frames(w, i)
         idx = [frames.index(f) for f in win]
         if win != cur:
             c2.anchor_set(0, win, torch.cat([akd[j * G:(j + 1) * G] for j in idx]).contiguous(),
