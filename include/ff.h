@@ -355,6 +355,24 @@ ff_status ff_packed_attention_bwd(const ff_packed_desc* desc, const void* q, con
                                   float softmax_scale, void* workspace, size_t workspace_bytes,
                                   void* stream);
 
+/* ff_packed_attention_bwd without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, serving or
+ * training loops, harnesses that forbid hipMalloc).  rowsum(dO * O) goes to a
+ * 64 MiB scratch array that the library holds in device memory, one per
+ * device, from the first call on that device until the process ends; the
+ * call itself allocates nothing.  Same arguments, results and errors as
+ * ff_packed_attention_bwd, plus FF_ERR_UNSUPPORTED when n_chunks *
+ * chunk_tokens * num_heads * 4 bytes exceed 64 MiB.  Every call on one device
+ * shares that device's scratch: calls that overlap in time on one device
+ * (two streams, two threads) race and give wrong gradients; calls on one
+ * stream are ordered and safe. */
+ff_status ff_packed_attention_bwd_static(const ff_packed_desc* desc, const void* q, const void* k,
+                                         const void* v, const void* anchor_k,
+                                         const void* anchor_v, const void* out, const void* dout,
+                                         const float* lse, void* dq, void* dk, void* dv,
+                                         void* d_anchor_k, void* d_anchor_v, float softmax_scale,
+                                         void* stream);
+
 /* Anchor partition of a clip of L latent frames with anchor spacing delta
  * (Eq. anchor-infill-partition): P = {m * delta : m * delta < L} u {L - 1},
  * ascending.  Writes |P| indices to out (host, `capacity` entries) and |P| to

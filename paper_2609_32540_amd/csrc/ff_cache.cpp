@@ -19,6 +19,7 @@
 #include <cstdio>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -758,13 +759,48 @@ size_t ff_packed_attention_bwd_workspace(const ff_packed_desc* desc) {
   return size_t(desc->n_chunks) * desc->chunk_tokens * desc->num_heads * sizeof(float);
 }
 
-ff_status ff_packed_attention_bwd(const ff_packed_desc* desc, const void* q, const void* k,
-                                  const void* v, const void* anchor_k, const void* anchor_v,
-                                  const void* out, const void* dout, const float* lse, void* dq,
-                                  void* dk, void* dv, void* d_anchor_k, void* d_anchor_v,
-                                  float softmax_scale, void* workspace, size_t workspace_bytes,
-                                  void* stream) {
-  return no_throw([&]() -> ff_status {
+}  // extern "C"
+
+namespace {
+
+// Scratch of ff_packed_attention_bwd_static: rowsum(dO * O) of up to
+// kStaticScratchBytes / 4 (token, head) rows.  Every device the library runs
+// the entry point on holds one copy until the process ends.  In host code the
+// name is only a stand-in: the device address comes from hipGetSymbolAddress.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+__device__ __align__(256) static unsigned char scratch[kStaticScratchBytes];
+
+struct StaticScratch {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t err = hipSuccess;
+};
+StaticScratch g_static_scratch[64];
+
+// Device address of `scratch` on the current device, looked up once per device.
+ff_status static_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(FF_ERR_UNSUPPORTED, "device %d out of range", dev);
+  StaticScratch& s = g_static_scratch[dev];
+  std::call_once(s.once, [&s] {
+    s.err = hipGetSymbolAddress(&s.ptr, HIP_SYMBOL(scratch));
+    if (s.err == hipSuccess && s.ptr == nullptr) s.err = hipErrorInvalidSymbol;
+  });
+  if (s.err != hipSuccess) return hip_status(s.err, "hipGetSymbolAddress(scratch)");
+  *ptr = s.ptr;
+  return ok();
+}
+
+// Both backward entry points: the workspace is the caller's, or the static
+// scratch of the current device when use_static is set.
+ff_status packed_bwd_impl(const ff_packed_desc* desc, const void* q, const void* k,
+                          const void* v, const void* anchor_k, const void* anchor_v,
+                          const void* out, const void* dout, const float* lse, void* dq, void* dk,
+                          void* dv, void* d_anchor_k, void* d_anchor_v, float softmax_scale,
+                          void* workspace, size_t workspace_bytes, bool use_static, void* stream) {
+  {
     ff::PackedPlan plan;
     ff_status st = make_packed_plan(desc, q, k, v, anchor_k, anchor_v, out, softmax_scale, &plan);
     if (st != FF_OK) return st;
@@ -772,22 +808,27 @@ ff_status ff_packed_attention_bwd(const ff_packed_desc* desc, const void* q, con
     if (d.dtype != FF_DT_BF16) return fail(FF_ERR_UNSUPPORTED, "the backward pass is bf16 only");
     if (d.n_anchor_frames > 64)
       return fail(FF_ERR_UNSUPPORTED, "the backward pass takes at most 64 anchor frames");
-    if (!dout || !lse || !dq || !dk || !dv || !workspace)
+    if (!dout || !lse || !dq || !dk || !dv || (!workspace && !use_static))
       return fail(FF_ERR_INVALID_ARG, "dout, lse, dq, dk, dv and workspace must be non-NULL");
     if (d.n_anchor_frames > 0 && (!d_anchor_k || !d_anchor_v))
       return fail(FF_ERR_INVALID_ARG, "d_anchor_k / d_anchor_v must be non-NULL with anchor frames");
     if (check_aligned(dout, "dout") != FF_OK || check_aligned(dq, "dq") != FF_OK ||
         check_aligned(dk, "dk") != FF_OK || check_aligned(dv, "dv") != FF_OK ||
-        check_aligned(workspace, "workspace") != FF_OK ||
+        (!use_static && check_aligned(workspace, "workspace") != FF_OK) ||
         (d.n_anchor_frames > 0 && (check_aligned(d_anchor_k, "d_anchor_k") != FF_OK ||
                                    check_aligned(d_anchor_v, "d_anchor_v") != FF_OK)))
       return FF_ERR_INVALID_ARG;
     if (reinterpret_cast<uintptr_t>(lse) % 4 != 0) return fail(FF_ERR_INVALID_ARG, "lse misaligned");
     const size_t need = ff_packed_attention_bwd_workspace(desc);
-    if (workspace_bytes < need)
+    if (use_static && need > kStaticScratchBytes)
+      return fail(FF_ERR_UNSUPPORTED,
+                  "%zu bytes of scratch needed (n_chunks * chunk_tokens * num_heads floats); "
+                  "the static scratch holds %zu",
+                  need, kStaticScratchBytes);
+    if (!use_static && workspace_bytes < need)
       return fail(FF_ERR_BUFFER, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
     // chunks that see each anchor frame, as runs of consecutive chunks
-    std::vector<std::array<uint8_t, 16>> frame_runs(std::max(d.n_anchor_frames, 1));
+    std::array<std::array<uint8_t, 16>, 64> frame_runs;
     for (int f = 0; f < d.n_anchor_frames; ++f) {
       std::fill(frame_runs[f].begin(), frame_runs[f].end(), uint8_t(0));
       int n = 0;
@@ -813,12 +854,45 @@ ff_status ff_packed_attention_bwd(const ff_packed_desc* desc, const void* q, con
         c = e;
       }
     }
+    if (use_static) {
+      st = static_scratch(&workspace);
+      if (st != FF_OK) return st;
+    }
     hipError_t e = ff::launch_attention_bwd_bf16(
         q, out, dout, lse, static_cast<float*>(workspace), dq, dk, dv, d_anchor_k, d_anchor_v,
         d.num_heads, d.head_dim, softmax_scale, plan,
         reinterpret_cast<const uint8_t(*)[16]>(frame_runs.data()), d.n_anchor_frames,
         static_cast<hipStream_t>(stream));
     return hip_status(e, "packed_attention_bwd launch");
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+ff_status ff_packed_attention_bwd(const ff_packed_desc* desc, const void* q, const void* k,
+                                  const void* v, const void* anchor_k, const void* anchor_v,
+                                  const void* out, const void* dout, const float* lse, void* dq,
+                                  void* dk, void* dv, void* d_anchor_k, void* d_anchor_v,
+                                  float softmax_scale, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  return no_throw([&]() -> ff_status {
+    return packed_bwd_impl(desc, q, k, v, anchor_k, anchor_v, out, dout, lse, dq, dk, dv,
+                           d_anchor_k, d_anchor_v, softmax_scale, workspace, workspace_bytes,
+                           false, stream);
+  });
+}
+
+ff_status ff_packed_attention_bwd_static(const ff_packed_desc* desc, const void* q, const void* k,
+                                         const void* v, const void* anchor_k,
+                                         const void* anchor_v, const void* out, const void* dout,
+                                         const float* lse, void* dq, void* dk, void* dv,
+                                         void* d_anchor_k, void* d_anchor_v, float softmax_scale,
+                                         void* stream) {
+  return no_throw([&]() -> ff_status {
+    return packed_bwd_impl(desc, q, k, v, anchor_k, anchor_v, out, dout, lse, dq, dk, dv,
+                           d_anchor_k, d_anchor_v, softmax_scale, nullptr, 0, true, stream);
   });
 }
 

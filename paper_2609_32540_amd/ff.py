@@ -103,6 +103,9 @@ SIGNATURES = [
     ("ff_packed_attention_bwd", _I32, [ctypes.POINTER(PackedDesc), _VP, _VP, _VP, _VP, _VP, _VP,
                                        _VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_float, _VP,
                                        _SZ, _VP]),
+    ("ff_packed_attention_bwd_static", _I32, [ctypes.POINTER(PackedDesc), _VP, _VP, _VP, _VP, _VP,
+                                              _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP,
+                                              ctypes.c_float, _VP]),
     ("ff_anchor_partition", _I32, [_I32, _I32, _PI32, _I32, _PI32]),
     ("ff_anchor_window", _I32, [_I64, _I32, _I32, _I32, _PI32, _PI32]),
     ("ff_anchor_flank", _I32, [_I64, _I32, _I32, _I32, _PI32, _PI32]),
@@ -494,6 +497,33 @@ def packed_attention_bwd(q, k, v, out, dout, lse, *, n_chunks: int, window: int,
         dak.data_ptr() if dak is not None else None, dav.data_ptr() if dav is not None else None,
         ctypes.c_float(scale), ws.data_ptr(), ws.numel(), _stream_handle(dev, stream)))
     return dq, dk, dv, dak, dav
+
+
+def packed_attention_bwd_static(q, k, v, out, dout, lse, dq, dk, dv, d_anchor_k=None,
+                                d_anchor_v=None, *, n_chunks: int, window: int, anchor_k=None,
+                                anchor_v=None, frame_tokens: int = 0, anchors_of_chunk=None,
+                                scale: Optional[float] = None,
+                                stream: Optional[torch.cuda.Stream] = None) -> None:
+    """ff_packed_attention_bwd_static: the backward into caller-provided gradients,
+    its scratch in the library's static device array (this call allocates no
+    device memory)."""
+    desc, table, akp, avp, shape, n_frames = _packed_desc(q, n_chunks, window, anchor_k, anchor_v,
+                                                          frame_tokens, anchors_of_chunk)
+    dev, dt = q.device, q.dtype
+    ptrs = [_dense(t, shape, dt, dev, n) for t, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out"),
+                                                      (dout, "dout"), (dq, "dq"), (dk, "dk"),
+                                                      (dv, "dv"))]
+    lp = _dense(lse, shape[:2], torch.float32, dev, "lse")
+    dak = dav = None
+    if anchor_k is not None:
+        a_shape = tuple(anchor_k.shape)
+        dak = _dense(d_anchor_k, a_shape, dt, dev, "d_anchor_k")
+        dav = _dense(d_anchor_v, a_shape, dt, dev, "d_anchor_v")
+    if scale is None:
+        scale = 1.0 / math.sqrt(shape[2])
+    _check(lib().ff_packed_attention_bwd_static(
+        ctypes.byref(desc), ptrs[0], ptrs[1], ptrs[2], akp, avp, ptrs[3], ptrs[4], lp,
+        ptrs[5], ptrs[6], ptrs[7], dak, dav, ctypes.c_float(scale), _stream_handle(dev, stream)))
 
 
 def anchor_partition(L: int, delta: int) -> List[int]:

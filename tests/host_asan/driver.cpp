@@ -187,6 +187,13 @@ static void packed_paths() {
   EXPECT(ff_packed_attention(&pd, t, t, t, t, t, t, 0.1f, nullptr, nullptr) == FF_OK);
   EXPECT(ff_packed_attention_bwd(&pd, t, t, t, t, t, t, t, reinterpret_cast<float*>(t), t, t, t,
                                  t, t, 0.1f, t, 1 << 20, nullptr) == FF_ERR_UNSUPPORTED);
+  EXPECT(ff_packed_attention_bwd_static(&pd, t, t, t, t, t, t, t, reinterpret_cast<float*>(t), t,
+                                        t, t, t, t, 0.1f, nullptr) == FF_ERR_UNSUPPORTED);
+  // beyond the 64 MiB static scratch: rejected before the device is touched
+  ff_packed_desc big = {64, 10800, 40, 128, 4, 3600, 0, FF_DT_BF16, nullptr};
+  EXPECT(ff_packed_attention_bwd_static(&big, t, t, t, nullptr, nullptr, t, t,
+                                        reinterpret_cast<float*>(t), t, t, t, nullptr, nullptr,
+                                        0.1f, nullptr) == FF_ERR_UNSUPPORTED);
 }
 
 static int32_t forward_calls = 0;

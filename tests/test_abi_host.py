@@ -34,7 +34,7 @@ def desc(**kw):
 def test_library_exports_every_header_symbol():
     L = ff.lib()
     names = header_functions()
-    assert len(names) == 26
+    assert len(names) == 27
     for n in names:
         assert hasattr(L, n), n
     assert {n for n, _, _ in ff.SIGNATURES} == set(names)
@@ -198,6 +198,23 @@ def test_packed_pointer_and_table_validation():
     # a chunk window wider than 4 GiB of bytes
     big = packed_desc(n_chunks=8, chunk_tokens=1 << 20, num_heads=40, head_dim=128, window=4)
     assert packed_call(big) == 5
+
+
+def test_static_backward_rejects_inputs_beyond_its_scratch():
+    # rowsum(dO * O) of 64 x 10800 x 40 (token, head) rows is 105 MiB, beyond the
+    # 64 MiB static scratch: rejected on the host, before any device call
+    L = ff.lib()
+    lse = ctypes.cast(FAKE_DEV, ctypes.c_void_p)
+
+    def call(d):
+        return L.ff_packed_attention_bwd_static(ctypes.byref(d), FAKE_DEV, FAKE_DEV, FAKE_DEV, None,
+                                                None, FAKE_DEV, FAKE_DEV, lse, FAKE_DEV, FAKE_DEV,
+                                                FAKE_DEV, None, None, ctypes.c_float(0.125), None)
+    big = packed_desc(n_chunks=64, chunk_tokens=10800, num_heads=40, head_dim=128, window=4)
+    assert call(big) == 5
+    assert "static scratch" in L.ff_last_error().decode()
+    assert call(packed_desc(dtype=ff.FF_DT_F32)) == 5                 # bf16 only, as the other entry
+    assert call(packed_desc(head_dim=96)) == 5
 
 
 # ----------------------------------------------------------------------
