@@ -11,12 +11,21 @@ full, so each step is a steady-state chunk-stage.  Inputs are synthetic
 Infinity Cache does not hold the previous layer's data.
 
 Prints one JSON line.  `value` is attention TFLOP/s over the whole timed
-region (attention FLOPs of every step / wall time of the steps, RoPE and
-publish included).  Events recorded between the launches of every layer inside
-the timed region give each kernel's average launch duration, from which the
-roofline of the attention kernel is taken; its HBM traffic comes from the
-counter summary under profiles/ when that summary was taken on the current
-kernel source.  The CPU oracle baseline is attached.
+region of the headline workload (attention FLOPs of every step / wall time of
+the steps, RoPE and publish included).  Events recorded between the launches
+of every layer inside the timed region give each kernel's average launch
+duration, from which the roofline of the attention kernel is taken; its HBM
+traffic comes from the counter summary under profiles/ when that summary was
+taken on the current kernel source.  Beside the headline:
+  configs        the same steps on the other chunk-stage workloads;
+  long_horizon   the 87-chunk clip from empty rings, every chunk at every stage
+                 and layer, anchor-set updates inside the timed region, timed
+                 per chunk;
+  kv_publish_cold / rope3d_cold  the streaming kernels on inputs that no
+                 kernel has touched since the previous step;
+  packed_clip_attention, wavefront_clip, cpu_baseline.
+`--only` runs the named workload's timed region alone (for per-workload
+kernel traces).
 
 `--copy-calibration` instead runs only a plain device copy of 1 GiB three
 times: the reference dispatch that scales the FETCH_SIZE / WRITE_SIZE counters.
@@ -28,6 +37,7 @@ import hashlib
 import json
 import math
 import os
+import subprocess
 import sys
 import time
 
@@ -59,7 +69,7 @@ def log(msg: str) -> None:
 class Workspace:
     """Cache, per-layer input buffers and the step schedule of one workload."""
 
-    def __init__(self, w: synth.Workload, seed: int = 0):
+    def __init__(self, w: synth.Workload, seed: int = 0, prefill: bool = True):
         self.w = w
         dev = torch.device("cuda", 0)
         self.dev = dev
@@ -85,11 +95,12 @@ class Workspace:
         self.anchor_v = [randn(a_shape) for _ in range(w.layers)]
         self.anchor_frames = None
         # fill every ring with W chunks (chunks 0 .. W-1) so the steps run at steady state
+        first = w.ring_chunks if prefill else 0
         for s in range(w.stages):
             for l in range(w.layers):
-                for c in range(w.ring_chunks):
+                for c in range(first):
                     self.cache.kv_publish(s, l, c, self.k[l], self.v[l])
-        self.next = (w.ring_chunks, 0)  # (chunk, stage) of the next step
+        self.next = (first, 0)  # (chunk, stage) of the next step
         torch.cuda.synchronize()
 
     def kv_tokens(self, chunk: int) -> int:
@@ -375,7 +386,174 @@ def cpu_baseline(w: synth.Workload, target_s: float = 12.0) -> dict:
             "sample": f"{n} x (1 head x {rows} queries x {nkv} keys x d {d}) of the float64 oracle "
                       f"attention, {el:.1f} s; full chunk-stage = {w.heads * w.layers} heads x "
                       f"{w.chunk_tokens} queries",
-            "seconds": round(el, 2)}
+            "seconds": round(el, 2), "threads_used": int(threads), **host_cpu()}
+
+
+def measure_steps(w: synth.Workload, steps: int, warmup: int) -> dict:
+    """Warm-up, then `steps` timed chunk-stage steps with per-kernel events,
+    then each layer's publish once more on cold inputs."""
+    t0 = time.time()
+    ws = Workspace(w)
+    log(f"{w.name}: {ws.cache.nbytes / 2**30:.1f} GiB cache, rings filled ({time.time() - t0:.1f} s)")
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        ws.step()
+    torch.cuda.synchronize()
+    # timed region: the steps bracketed by events on the launch stream, with
+    # events between the kernels of every layer for the per-kernel durations
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(w.layers)]
+              for _ in range(steps)]
+    chunks, flops = [], 0.0
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(steps):
+        chunks.append(ws.next[0])
+        flops += ws.step(events[k])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    rope_ms, attn_ms, pub_ms, attn_flops = [], [], [], []
+    for k in range(steps):
+        for l in range(w.layers):
+            ev = events[k][l]
+            rope_ms.append(ev[0].elapsed_time(ev[1]))
+            attn_ms.append(ev[1].elapsed_time(ev[2]))
+            pub_ms.append(ev[2].elapsed_time(ev[3]))
+            attn_flops.append(ws.attn_flops(chunks[k]))
+    # cold publish: each layer's K/V were last touched a whole step ago (every
+    # other layer's kernels have streamed through the caches since)
+    chunk, stage = ws.next
+    cold = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(w.layers)]
+    for l in range(w.layers):
+        cold[l][0].record(stream)
+        ws.cache.kv_publish(stage, l, chunk, ws.k[l], ws.v[l])
+        cold[l][1].record(stream)
+    torch.cuda.synchronize()
+    pub_cold = float(np.mean([e[0].elapsed_time(e[1]) for e in cold]))
+    res = dict(ms_total=ms_total, flops=flops, chunks=chunks,
+               attn_ms=float(np.mean(attn_ms)), pub_ms=float(np.mean(pub_ms)),
+               rope_ms=float(np.mean(rope_ms)), pub_cold_ms=pub_cold,
+               attn_flops=float(np.mean(attn_flops)),
+               kv_tokens=ws.kv_tokens(chunks[-1]), anchor_frames=len(frames_of(w, chunks[-1])),
+               cache_gib=ws.cache.nbytes / 2**30)
+    del ws
+    torch.cuda.empty_cache()
+    return res
+
+
+def stream_bytes(w: synth.Workload) -> float:
+    """Algorithmic bytes of RoPE or publish on one chunk and layer: two
+    [chunk_tokens][heads][head_dim] tensors read once and written once."""
+    return 4.0 * w.chunk_tokens * w.heads * w.head_dim * (2 if w.dtype == "bf16" else 4)
+
+
+def summarize(w: synth.Workload, m: dict, steps: int) -> dict:
+    """Per-chunk-stage figures of one workload's timed steps."""
+    tf = m["attn_flops"] / (m["attn_ms"] * 1e-3) / 1e12
+    sb = stream_bytes(w)
+    gbs = {k: sb / (m[k] * 1e-3) / 1e9 for k in ("pub_ms", "rope_ms", "pub_cold_ms")}
+    target = m["attn_flops"] * w.layers / (0.5 * PEAK_BF16_TFLOPS * 1e12) * 1e3
+    value = m["flops"] / (m["ms_total"] * 1e-3) / 1e12
+    return {
+        "workload": w.name, "heads": w.heads, "head_dim": w.head_dim,
+        "grid": f"{w.grid_h}x{w.grid_w}", "chunk_tokens": w.chunk_tokens,
+        "kv_tokens": m["kv_tokens"], "ring_chunks": w.ring_chunks, "stages": w.stages,
+        "layers": w.layers, "anchor_frames": m["anchor_frames"], "steps": steps,
+        "ms_per_step": round(m["ms_total"] / steps, 3),
+        "tflops_step": round(value, 2),
+        "ms_attn_per_chunk_stage": round(m["attn_ms"] * w.layers, 3),
+        "ms_attn_target_at_50pct_peak": round(target, 3),
+        "ms_attn_publish_per_chunk_stage": round((m["attn_ms"] + m["pub_ms"]) * w.layers, 3),
+        "ms_rope_per_chunk_stage": round(m["rope_ms"] * w.layers, 3),
+        "attention": {"ms_per_launch": round(m["attn_ms"], 4), "tflops": round(tf, 2),
+                      "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2)},
+        "kv_publish": {"us_per_launch": round(m["pub_ms"] * 1e3, 2), "gbs": round(gbs["pub_ms"], 1),
+                       "pct_hbm_peak": round(100 * gbs["pub_ms"] / PEAK_HBM_GBS, 2),
+                       "inputs": "K/V just read by the attention launch"},
+        "kv_publish_cold": {"us_per_launch": round(m["pub_cold_ms"] * 1e3, 2),
+                            "gbs": round(gbs["pub_cold_ms"], 1),
+                            "pct_hbm_peak": round(100 * gbs["pub_cold_ms"] / PEAK_HBM_GBS, 2),
+                            "inputs": "K/V untouched since the previous step"},
+        "rope3d": {"us_per_launch": round(m["rope_ms"] * 1e3, 2), "gbs": round(gbs["rope_ms"], 1),
+                   "pct_hbm_peak": round(100 * gbs["rope_ms"] / PEAK_HBM_GBS, 2),
+                   "inputs": "Q/K untouched since the previous step"},
+    }
+
+
+def long_horizon(w: synth.Workload) -> dict:
+    """The whole clip from empty rings: chunk i at stages 0..S-1 over every
+    layer, i = 0 .. n_chunks-1, with every anchor-set update (RoPE of the new
+    anchor frames and their copy into each layer's segment) inside the timed
+    region.  Events at chunk boundaries give the per-chunk series."""
+    ws = Workspace(w, prefill=False)
+    stream = torch.cuda.current_stream()
+    # warm the code objects on a throw-away cache of the same shape
+    warm = Workspace(synth.small_workload("warm", heads=w.heads, head_dim=w.head_dim, grid_h=w.grid_h,
+                                          grid_w=w.grid_w, ring_chunks=w.ring_chunks, stages=1,
+                                          layers=1, n_chunks=2, anchor_rule="fixed:0"))
+    warm.step()
+    del warm
+    torch.cuda.synchronize()
+    n, S = w.n_chunks, w.stages
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    flops_chunk, updates, prev = [], [], None
+    ev[0].record(stream)
+    for i in range(n):
+        fr = frames_of(w, i)
+        if fr != prev:
+            updates.append(i)
+            prev = fr
+        f = 0.0
+        for _ in range(S):
+            f += ws.step()
+        flops_chunk.append(f)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
+    total = float(sum(ms))
+    tf = sum(flops_chunk) / (total * 1e-3) / 1e12
+    kv = [ws.kv_tokens(i) for i in range(n)]
+    log(f"long horizon {w.name}: {n} chunks x {S} stages x {w.layers} layers in {total:.0f} ms "
+        f"= {tf:.1f} TFLOP/s, {len(updates)} anchor updates")
+    del ws
+    torch.cuda.empty_cache()
+    return {"workload": w.name, "chunks": n, "stages": S, "layers": w.layers,
+            "ms_total": round(total, 2), "tflops": round(tf, 2),
+            "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2),
+            "anchor_update_chunks": updates,
+            "ms_per_chunk": [round(x, 3) for x in ms],
+            "kv_tokens_per_chunk": kv,
+            "note": "ms_per_chunk: all stages and layers of the chunk (RoPE, attention, publish, "
+                    "and the anchor update at the listed chunks)"}
+
+
+def host_cpu() -> dict:
+    """CPU model and core counts of this host (lscpu), and the CPUs this
+    process may run on."""
+    info = {}
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        kv = dict(line.split(":", 1) for line in out.splitlines() if ":" in line)
+        kv = {k.strip(): v.strip() for k, v in kv.items()}
+        info["cpu_model"] = kv.get("Model name")
+        sockets = int(kv.get("Socket(s)", "0") or 0)
+        per = int(kv.get("Core(s) per socket", "0") or 0)
+        info["physical_cores"] = sockets * per if sockets and per else None
+        info["logical_cpus"] = int(kv.get("CPU(s)", "0") or 0) or None
+    except (OSError, ValueError, subprocess.SubprocessError):
+        pass
+    try:
+        info["cpus_allowed"] = len(os.sched_getaffinity(0))
+    except OSError:
+        pass
+    try:
+        quota, period = open("/sys/fs/cgroup/cpu.max").read().split()
+        if quota != "max":
+            info["cgroup_cpu_quota"] = round(int(quota) / int(period), 2)
+    except (OSError, ValueError):
+        pass
+    return info
 
 
 def main() -> int:
@@ -384,6 +562,13 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=8)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="14b-720p", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--configs", default="1.3b-480p,14b-480p",
+                    help="other chunk-stage workloads to time beside the headline ('' for none)")
+    ap.add_argument("--config-steps", type=int, default=4)
+    ap.add_argument("--long-horizon", default="1.3b-480p-long",
+                    help="workload of the per-chunk clip series ('' to skip)")
+    ap.add_argument("--only", action="store_true",
+                    help="time only --workload (a clip series for a long-horizon workload)")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--no-packed", action="store_true",
                     help="skip the packed whole-clip attention measurement")
@@ -406,62 +591,28 @@ def main() -> int:
         print("the benchmark workloads are the bf16 ones", file=sys.stderr)
         return 2
     ff.lib()
+    if args.only and w.anchor_rule.startswith("flank"):
+        print(json.dumps({"long_horizon": long_horizon(w)}), flush=True)
+        return 0
     log(f"workload {w.name}: {w.heads} heads x {w.head_dim}, {w.chunk_tokens} queries, "
         f"{w.layers} layers, {w.stages} stages")
-    t0 = time.time()
-    ws = Workspace(w)
-    log(f"allocated {ws.cache.nbytes / 2**30:.1f} GiB cache, rings filled ({time.time() - t0:.1f} s)")
-    stream = torch.cuda.current_stream()
-
-    for _ in range(args.warmup):
-        ws.step()
-    torch.cuda.synchronize()
-    log("warmup done")
-
-    # timed region: K steps bracketed by events on the launch stream, with
-    # events between the kernels of every layer for the per-kernel durations
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    events, chunks = [], []
-    for _ in range(args.steps):
-        events.append([[torch.cuda.Event(enable_timing=True) for _ in range(4)]
-                       for _ in range(w.layers)])
-    flops = 0.0
-    torch.cuda.synchronize()
-    start.record(stream)
-    for k in range(args.steps):
-        chunks.append(ws.next[0])
-        flops += ws.step(events[k])
-    stop.record(stream)
-    torch.cuda.synchronize()
-    ms_total = start.elapsed_time(stop)
-    ms_per_step = ms_total / args.steps
-    value = flops / (ms_total * 1e-3) / 1e12
-    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {value:.1f} TFLOP/s")
-
-    rope_ms, attn_ms, pub_ms, attn_flops = [], [], [], []
-    for k in range(args.steps):
-        for l in range(w.layers):
-            ev = events[k][l]
-            rope_ms.append(ev[0].elapsed_time(ev[1]))
-            attn_ms.append(ev[1].elapsed_time(ev[2]))
-            pub_ms.append(ev[2].elapsed_time(ev[3]))
-            attn_flops.append(ws.attn_flops(chunks[k]))
-    attn_avg = float(np.mean(attn_ms))
-    pub_avg = float(np.mean(pub_ms))
-    rope_avg = float(np.mean(rope_ms))
-    attn_achieved = float(np.mean(attn_flops)) / (attn_avg * 1e-3) / 1e12
-    elem = 2
-    pub_bytes = 4.0 * w.chunk_tokens * w.heads * w.head_dim * elem
-    rope_bytes = 4.0 * w.chunk_tokens * w.heads * w.head_dim * elem
-    pub_gbs = pub_bytes / (pub_avg * 1e-3) / 1e9
-    rope_gbs = rope_bytes / (rope_avg * 1e-3) / 1e9
-    log(f"attention {attn_avg:.3f} ms/launch = {attn_achieved:.1f} TFLOP/s; publish {pub_avg*1e3:.1f} us "
-        f"= {pub_gbs:.0f} GB/s; rope {rope_avg*1e3:.1f} us = {rope_gbs:.0f} GB/s")
+    m = measure_steps(w, args.steps, args.warmup)
+    head = summarize(w, m, args.steps)
+    value = m["flops"] / (m["ms_total"] * 1e-3) / 1e12
+    attn_tf = head["attention"]["tflops"]
+    log(f"timed {args.steps} steps: {head['ms_per_step']:.3f} ms/step, {value:.1f} TFLOP/s; "
+        f"attention {m['attn_ms']:.3f} ms/launch = {attn_tf:.1f} TFLOP/s; publish "
+        f"{head['kv_publish']['gbs']:.0f} GB/s (cold {head['kv_publish_cold']['gbs']:.0f}); "
+        f"rope {head['rope3d']['gbs']:.0f} GB/s")
 
     traffic, traffic_src = measured_traffic(w.name)
     # compulsory bytes of one launch: Q, K, V, O of the chunk once each, every
     # history and anchor key/value once (the whole read set, all heads)
-    attn_bytes = elem * w.heads * w.head_dim * (2 * w.chunk_tokens + 2 * ws.kv_tokens(chunks[-1]))
+    elem = 2
+    attn_bytes = elem * w.heads * w.head_dim * (2 * w.chunk_tokens + 2 * m["kv_tokens"])
+    config = {k: head[k] for k in ("workload", "heads", "head_dim", "grid", "chunk_tokens",
+                                   "kv_tokens", "ring_chunks", "stages", "layers",
+                                   "anchor_frames")}
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -469,42 +620,44 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 3),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": w.name, "heads": w.heads, "head_dim": w.head_dim,
-                   "grid": f"{w.grid_h}x{w.grid_w}", "chunk_tokens": w.chunk_tokens,
-                   "kv_tokens": ws.kv_tokens(w.ring_chunks + 1), "ring_chunks": w.ring_chunks,
-                   "stages": w.stages, "layers": w.layers, "anchor_frames": 3},
+        "config": config,
         "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
-        "ms_attn_publish_per_chunk_stage": round((attn_avg + pub_avg) * w.layers, 3),
-        "ms_rope_per_chunk_stage": round(rope_avg * w.layers, 3),
-        "kernels": {
-            "attention": {"ms_per_launch": round(attn_avg, 4), "tflops": round(attn_achieved, 2),
-                          "pct_bf16_peak": round(100 * attn_achieved / PEAK_BF16_TFLOPS, 2)},
-            "kv_publish": {"us_per_launch": round(pub_avg * 1e3, 2), "gbs": round(pub_gbs, 1),
-                           "pct_hbm_peak": round(100 * pub_gbs / PEAK_HBM_GBS, 2)},
-            "rope3d": {"us_per_launch": round(rope_avg * 1e3, 2), "gbs": round(rope_gbs, 1),
-                       "pct_hbm_peak": round(100 * rope_gbs / PEAK_HBM_GBS, 2)},
-        },
-        "roofline": {"bound": "mfma", "achieved": round(attn_achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(attn_achieved / PEAK_BF16_TFLOPS, 4),
+        "ms_attn_per_chunk_stage": head["ms_attn_per_chunk_stage"],
+        "ms_attn_target_at_50pct_peak": head["ms_attn_target_at_50pct_peak"],
+        "ms_attn_publish_per_chunk_stage": head["ms_attn_publish_per_chunk_stage"],
+        "ms_rope_per_chunk_stage": head["ms_rope_per_chunk_stage"],
+        "kernels": {k: head[k] for k in ("attention", "kv_publish", "kv_publish_cold", "rope3d")},
+        "roofline": {"bound": "mfma", "achieved": attn_tf, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tf / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "traffic_unit": "HBM bytes per launch",
                      "traffic_source": traffic_src,
                      "algorithmic_bytes_per_launch": attn_bytes},
     }
-    del ws
-    torch.cuda.empty_cache()
-    if not args.no_packed:
-        result["packed_clip_attention"] = packed_clip(w)
-    if not args.no_wavefront:
-        result["wavefront_clip"] = wavefront_clip()
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle")
-        result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    if not args.only:
+        result["configs"] = {}
+        for name in [c for c in args.configs.split(",") if c]:
+            wc = synth.WORKLOADS[name]
+            mc = measure_steps(wc, args.config_steps, 1)
+            result["configs"][name] = summarize(wc, mc, args.config_steps)
+            sc = result["configs"][name]
+            log(f"{name}: attention {sc['ms_attn_per_chunk_stage']:.2f} ms per chunk-stage "
+                f"({sc['attention']['pct_bf16_peak']:.1f} % of peak; target "
+                f"{sc['ms_attn_target_at_50pct_peak']:.2f} ms at 50 %)")
+        if args.long_horizon:
+            result["long_horizon"] = long_horizon(synth.WORKLOADS[args.long_horizon])
+        if not args.no_packed:
+            result["packed_clip_attention"] = packed_clip(w)
+        if not args.no_wavefront:
+            result["wavefront_clip"] = wavefront_clip()
+        if not args.no_cpu_baseline:
+            log("timing the CPU oracle")
+            result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(result), flush=True)
     return 0
 
