@@ -7,14 +7,17 @@
 // is partial (its missing keys are masked to -inf): no tile straddles two
 // segments and no empty slot is touched.
 //
-// Products, per 32-key block (two per tile):
-//   S^T = K Q^T     v_mfma_f32_32x32x16_bf16; A = K rows read from LDS, B = the
+// Products, per 32-key block (two per tile), all on v_mfma_f32_16x16x32_bf16
+// (16 x 16 outputs, 32-deep sums):
+//   S^T = K Q^T     four 16 x 16 tiles (key half kh x query half qh), four
+//                   32-wide d slices each; A = K rows read from LDS, B = the
 //                   wave's Q^T, held in registers for the whole loop.
-//   softmax         the accumulator layout of S^T puts one query column in each
-//                   lane (half of a 32-key block; the other half is in lane ^ 32),
-//                   so the row sums stay in-lane until the end.  p = exp2(s c -
-//                   m) with c = scale * log2 e applied in float32 (one fma; Q is
-//                   not rounded again after scaling).  The reference max m is the
+//   softmax         lane (n, g) = (lane % 16, lane / 16) holds, for query n of
+//                   each query half, keys 4g .. 4g+3 of each key half, so a
+//                   query's row sum stays in-lane until a final reduction over
+//                   the four lane groups.  p = exp2(s c - m) with c = scale *
+//                   log2 e applied in float32 (one fma; Q is not rounded again
+//                   after scaling).  The reference max m is the
 //                   first block's column max and is only raised when a block's
 //                   probabilities sum past kSumLimit (every kept probability is
 //                   then at most kSumLimit, and infinities from scores far above
@@ -22,10 +25,12 @@
 //                   recomputed from LDS, O and l rescaled and its probabilities
 //                   redone.  The result is exact for any reference, since the
 //                   final sum uses the same one; no column max is taken per block.
-//   O^T += V^T P^T  A = V^T, read from the row-major V tile with the gfx950
+//   O^T += V^T P^T  16-row d tiles x query halves, one 32-deep sum per block;
+//                   A = V^T, read from the row-major V tile with the gfx950
 //                   transposing LDS read (ds_read_b64_tr_b16); B = P^T, the
-//                   softmax registers rounded to bf16 in place.  The keys of each
-//                   8-key operand are chosen to match the accumulator layout.
+//                   softmax registers rounded to bf16 in place.  The sum runs
+//                   over the keys in the order the softmax registers hold them
+//                   (lane group g: keys 4g .. 4g+3, then 16+4g .. 16+4g+3).
 // Software pipeline over blocks b: A(b) computes S^T of block b+1 on the matrix
 // core beside the exponentials of block b; B(b) checks block b's sum, adds
 // block b into O^T and masks block b+1 if it is partial.  Waves w and w + 4
@@ -39,11 +44,15 @@
 // before barrier t.  Barrier t waits only for the copy of tile t+1, so each
 // copy has a whole step to land.  The copies are issued from inline assembly
 // and waited for explicitly, so the compiler does not add its own conservative
-// waits for them; the loops are unrolled by five so every slot reference is
-// static.
-// Tile rows are stored without padding, with an XOR swizzle of their 16-byte
-// chunks that keeps both the K reads and the transposing V reads free of bank
-// conflicts on the 64-bank LDS.
+// waits for them.  Every LDS read is a per-lane base plus immediates except
+// for the slot base, added once per phase, so the tile loop stays rolled
+// (the kernel's hot code is a few KB).
+// The tiles are stored without padding in layouts chosen for their reads: a K
+// tile chunk-major per 16 keys (one 256-byte line per 16-byte chunk of 16
+// keys), a V tile d-blocked (one 256-byte line per 8 keys and 16-wide d tile).
+// Each 16-byte K read of a quarter-wave and each transposing V read of a
+// half-wave then takes exactly one line, free of bank conflicts on the
+// 64-bank LDS, and the d slices and d tiles differ by immediate offsets.
 // Workgroups are renumbered so that consecutive Q tiles of one head land on
 // the same XCD (the hardware deals workgroups to the 8 XCDs round robin) and
 // share that XCD's L2 for the head's K/V (a packed clip deals whole (chunk,
@@ -75,8 +84,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kCB = 1;                      // 32-query column blocks per wave
-constexpr int kWaveQ = 32 * kCB;            // queries per wave
+constexpr int kQH = 2;                      // 16-query halves per wave
+constexpr int kWaveQ = 16 * kQH;            // queries per wave
 constexpr int kBlockQ = kWaves * kWaveQ;    // queries per workgroup
 constexpr int kBK = 64;                     // keys per tile
 constexpr int kXcds = 8;
@@ -88,8 +97,8 @@ constexpr int kCopyWaves = kWaves / 2;
 
 template <int D>
 struct Cfg {
-  static constexpr int KS = D / 16;          // 16-wide d slices of S^T = K Q^T
-  static constexpr int DB = D / 32;          // 32-row blocks of O^T
+  static constexpr int KS = D / 32;          // 32-wide d slices of S^T = K Q^T
+  static constexpr int DT = D / 16;          // 16-row d tiles of O^T
   static constexpr int ROWB = 2 * D;         // bytes per K/V row in LDS
   static constexpr int CPR = D / 8;          // 16-byte chunks per row
   static constexpr int RPB = 1024 / ROWB;    // rows per 1 KB wave copy
@@ -97,22 +106,10 @@ struct Cfg {
   static constexpr int BLOCKS_PER_WAVE = BLOCKS / kCopyWaves;   // copies by waves 0 .. kCopyWaves-1
   static constexpr int TILE = kBK * ROWB;    // bytes of one K (or V) tile
   static constexpr int SLOT = 2 * TILE;      // K tile then V tile
+  static constexpr int VGB = D / 64;         // 1 KB blocks per 8-row group of a V tile
+  static constexpr int KGB = D / 32;         // 1 KB blocks per 16-row group of a K tile
   static_assert(BLOCKS % kCopyWaves == 0, "every copying wave copies the same number of 1 KB blocks");
 };
-
-// XOR swizzle of the 16-byte chunks of tile row r, for an LDS that serves
-// 256 bytes per clock (64 banks): a 16-lane quarter of a 16-byte K read (16
-// consecutive rows, one chunk) and a 32-lane half of an 8-byte transposing V
-// read (4 rows x 4 adjacent chunks) must each touch 16 (resp. 32) distinct
-// 16-byte (8-byte) bank slots.  d = 128 (256-byte rows, 16 chunks): the row's
-// low two bits pick the chunk group and the next two the chunk inside it.
-// d = 64 (128-byte rows, 8 chunks, two rows per bank line): same idea on the
-// row bits above the line parity.
-template <int D>
-__device__ inline int swz(int r) {
-  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
-  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
-}
 
 // 16 bytes per lane from global memory (uniform base + per-lane byte offset)
 // straight into LDS at dst + 16 * lane.  Written out so that the compiler does
@@ -128,13 +125,19 @@ __device__ inline uint32_t pack_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
 }
 
-__device__ inline float max_across_halves(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+// max and sum over the lanes n, n + 16, n + 32, n + 48 (the four lane groups
+// holding one query's keys)
+__device__ inline float max_across_groups(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
-__device__ inline float sum_across_halves(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+__device__ inline float sum_across_groups(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
@@ -162,11 +165,8 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   constexpr bool kBatch = __is_same(Src, KvBatch);
   constexpr bool kSets = kPacked || kBatch;   // one read set per (chunk or item) of the grid
   using C = Cfg<D>;
-  __shared__ __attribute__((aligned(1024))) char lds0[C::SLOT];
-  __shared__ __attribute__((aligned(1024))) char lds1[C::SLOT];
-  __shared__ __attribute__((aligned(1024))) char lds2[C::SLOT];
-  __shared__ __attribute__((aligned(1024))) char lds3[C::SLOT];
-  __shared__ __attribute__((aligned(1024))) char lds4[C::SLOT];
+  __shared__ __attribute__((aligned(1024))) char lds[5 * C::SLOT];
+  auto slot = [&](int i) __attribute__((always_inline)) { return lds + i * C::SLOT; };
 
   // Workgroups b < tail.n_full run whole units (head, 256-query tile),
   // renumbered XCD-aware: hardware block b runs on XCD b % 8, so each XCD gets
@@ -217,33 +217,33 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform
   const int lane = tid & 63;
-  const int l32 = lane & 31;
-  const int half = lane >> 5;
+  const int l16 = lane & 15;
+  const int grp = lane >> 4;
 
-  // Q^T operand: lane (l32, half) of column block cb holds query
-  // q0 + 32 cb + l32, elements d = 16 s + 8 half .. +7 of slice s.
+  // Q^T operand: lane (l16, grp) of query half qh holds query q0 + 16 qh + l16,
+  // elements d = 32 s + 8 grp .. +7 of slice s.
   const int q0 = qt * kBlockQ + wave * kWaveQ;
-  bf16x8 qreg[kCB][C::KS];
+  bf16x8 qreg[kQH][C::KS];
 #pragma unroll
-  for (int cb = 0; cb < kCB; ++cb) {
-    const int qi = min(q0 + 32 * cb + l32, nq - 1);
-    const __bf16* qp = q + (int64_t(qi) * heads + head) * D + 8 * half;
+  for (int qh = 0; qh < kQH; ++qh) {
+    const int qi = min(q0 + 16 * qh + l16, nq - 1);
+    const __bf16* qp = q + (int64_t(qi) * heads + head) * D + 8 * grp;
 #pragma unroll
-    for (int s = 0; s < C::KS; ++s) qreg[cb][s] = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
+    for (int s = 0; s < C::KS; ++s) qreg[qh][s] = *reinterpret_cast<const bf16x8*>(qp + 32 * s);
   }
 
-  f32x16 o[kCB][C::DB];
+  // O^T tile (d tile dt, query half qh): lane (l16, grp) holds query
+  // q0 + 16 qh + l16 at d = 16 dt + 4 grp + j, j = 0 .. 3
+  f32x4 o[C::DT][kQH];
 #pragma unroll
-  for (int cb = 0; cb < kCB; ++cb)
+  for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
-    for (int db = 0; db < C::DB; ++db)
+    for (int qh = 0; qh < kQH; ++qh) o[dt][qh] = f32x4{};
+  float m_run[kQH], l_run[kQH];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) o[cb][db][j] = 0.0f;
-  float m_run[kCB], l_run[kCB];
-#pragma unroll
-  for (int cb = 0; cb < kCB; ++cb) {
-    m_run[cb] = 0.0f;       // reference max of the scaled logits (log2 units)
-    l_run[cb] = 0.0f;       // this lane's partial sum of probabilities
+  for (int qh = 0; qh < kQH; ++qh) {
+    m_run[qh] = 0.0f;       // reference max of the scaled logits (log2 units)
+    l_run[qh] = 0.0f;       // this lane's partial sum of probabilities
   }
 
   // Segment table in registers: lane i holds segment i's length, tokens-stride
@@ -286,20 +286,25 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     return c;
   };
 
-  // tile copy: 1 KB per wave instruction; lane -> (row, physical chunk).  A
-  // segment's rows are at most 2^31 bytes apart (the host limits a chunk to
+  // tile copy: 1 KB per wave instruction, lane l lands at 16 l of the block.
+  //   K tile, chunk-major per 16 rows: 16-row group G takes D / 32 blocks, and
+  //     in them one 256-byte line per 16-byte chunk c holding that chunk of rows
+  //     16 G .. 16 G + 15; block b = (G, m) holds the lines of chunks 4 m .. 4 m + 3,
+  //     so lane l carries row 16 G + l % 16, chunk 4 m + l / 16.
+  //   V tile, d-blocked: 8-row group G takes D / 64 blocks, and in them one
+  //     256-byte line per 16-wide d tile dt holding, for row 8 G + i, chunks
+  //     2 dt and 2 dt + 1 at 16 (2 i) and 16 (2 i + 1); block b = (G, H) holds
+  //     the lines of d tiles 4 H .. 4 H + 3, so lane l carries row 8 G + (l % 16) / 2,
+  //     chunk 8 H + 2 (l / 16) + l % 2.
+  // A segment's rows are at most 2^31 bytes apart (the host limits a chunk to
   // 2^31 elements), so each lane's source is a 32-bit byte offset from the
   // segment's (uniform) head base; rows past a partial tile's end re-read its
-  // last row, whose scores are masked.
-  int cp_row[C::BLOCKS_PER_WAVE], cp_choff[C::BLOCKS_PER_WAVE];
-#pragma unroll
-  for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
-    const int r = (wave * C::BLOCKS_PER_WAVE + i) * C::RPB + lane / C::CPR;
-    cp_row[i] = r;
-    cp_choff[i] = 16 * ((lane % C::CPR) ^ swz<D>(r));
-  }
+  // last row, whose scores are masked.  The per-lane offsets are recomputed per
+  // tile rather than held in registers across the loop.
   auto issue_tile = [&](char* base, Cursor c) __attribute__((always_inline)) {
     if (wave >= kCopyWaves) return;
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
     const int len = seg_len(c.sg);
     const uint32_t row_bytes = uint32_t(__builtin_amdgcn_readlane(int(sg_row_bytes), c.sg));
     const char* kb = reinterpret_cast<const char*>(readlane_u64(sg_k, c.sg));
@@ -307,81 +312,99 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     const bool partial = c.k0 + kBK > len;
 #pragma unroll
     for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
-      int tok = c.k0 + cp_row[i];
-      if (partial) tok = min(tok, len - 1);
-      const uint32_t off = uint32_t(tok) * row_bytes + uint32_t(cp_choff[i]);
-      const uint32_t dst = uint32_t(size_t(LDS_PTR(char, base))) + (wave * C::BLOCKS_PER_WAVE + i) * 1024;
-      lds_copy16(dst, kb, off);
-      lds_copy16(dst + C::TILE, vb, off);
+      const int blk = wave * C::BLOCKS_PER_WAVE + i;
+      const int kr = 16 * (blk / C::KGB) + (ln & 15);
+      const int kch = 4 * (blk % C::KGB) + (ln >> 4);
+      const int vr = 8 * (blk / C::VGB) + ((ln & 15) >> 1);
+      const int vch = 8 * (blk % C::VGB) + 2 * (ln >> 4) + (ln & 1);
+      int ktok = c.k0 + kr, vtok = c.k0 + vr;
+      if (partial) {
+        ktok = min(ktok, len - 1);
+        vtok = min(vtok, len - 1);
+      }
+      const uint32_t koff = uint32_t(ktok) * row_bytes + 16u * uint32_t(kch);
+      const uint32_t voff = uint32_t(vtok) * row_bytes + 16u * uint32_t(vch);
+      const uint32_t dst = uint32_t(size_t(LDS_PTR(char, base))) + blk * 1024;
+      lds_copy16(dst, kb, koff);
+      lds_copy16(dst + C::TILE, vb, voff);
     }
   };
 
   // LDS read addresses.  The swizzle only flips chunk bits that the row offset
   // leaves clear, so each read is (slot + immediate) + (lane base ^ constant):
-  //   K (A of S^T), row kb*32 + l32, chunk 2 ks + half: k_lane ^ (ks << 5), +8 KB for kb = 1
-  //     (both blocks share the swizzle: it depends on the row's low four bits only);
-  //   V (A of O^T, transposing read), lane group g = lane / 16 covers d block
-  //     32 db + 16 (g & 1) and key half (g >> 1); lane l' = lane % 16 reads key row
-  //     kbase + l' / 4 at d offset 4 (l' % 4): v_lane[lo/hi] ^ (db << 6) for D = 128
-  //     (chunk group = db), + (32 kb + 16 mh) rows.
-  int k_lane = l32 * C::ROWB + ((half ^ swz<D>(l32)) << 4);
-  const int g = lane >> 4;
-  const int lp = lane & 15;
-  const int v_row = 4 * (g >> 1) + (lp >> 2);               // row of the lo read within a 16-key group
-  const int v_dsub = 16 * (g & 1) + 4 * (lp & 3);            // d offset within a 32-d block
+  //   K (A of S^T), row 16 kh + l16, chunk 4 ks + grp: k_lane + 1024 ks + 16 ROWB kh
+  //     in the chunk-major K tile (a 16-lane quarter reads one whole 256-byte line);
+  //   V (A of O^T, transposing read), lane group grp reads key rows 4 grp .. 4 grp+3
+  //     (lo) and 16 + 4 grp .. +3 (hi) of the block, lane l16 the row 4 grp + l16 / 4
+  //     (+ 16) at d offset 4 (l16 % 4) of the d tile, and receives column l16 of the
+  //     four rows: v_lane[lo/hi] + 256 dt for d tile dt in the d-blocked V tile
+  //     (a 32-lane half reads one whole 256-byte line: no bank conflicts).
+  const int k_lane = 256 * grp + 16 * l16;
   int v_lane[2];
 #pragma unroll
   for (int hi = 0; hi < 2; ++hi) {
-    const int r = v_row + 8 * hi;
-    v_lane[hi] = r * C::ROWB + (((v_dsub >> 3) ^ swz<D>(r)) << 4) + (v_dsub & 7) * 2;
+    const int r = 16 * hi + 4 * grp + (l16 >> 2);
+    v_lane[hi] = (r >> 3) * (8 * C::ROWB) + ((2 * (r & 7) + ((l16 >> 1) & 1)) << 4) + 8 * (l16 & 1);
   }
-  // chunk bits flipped per d block: D = 128 has 4 chunks per 32-d block, D = 64 as well
-  constexpr int kVdbShift = 6;   // (4 chunks per db) << 4 bytes
 
-  // S^T of 32-key block kb of the tile at kt, both column blocks
-  auto s_blk = [&](const char* kt, int kb, f32x16 (&s)[kCB]) __attribute__((always_inline)) {
+  // S^T of 32-key block kb of the tile at kt: tile (kh, qh) = keys 16 kh .. +15 x
+  // queries 16 qh .. +15 of the wave; lane (l16, grp) register j holds key
+  // 16 kh + 4 grp + j of query 16 qh + l16
+  auto s_blk = [&](const char* kt, int kb, f32x4 (&s)[2][kQH]) __attribute__((always_inline)) {
     const char* kbase = kt + kb * 32 * C::ROWB;
 #pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kbase + (k_lane ^ (ks << 5)));
+    for (int ks = 0; ks < C::KS; ++ks)
 #pragma unroll
-      for (int cb = 0; cb < kCB; ++cb)
-        s[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[cb][ks], ks == 0 ? f32x16{} : s[cb],
-                                                        0, 0, 0);
-    }
+      for (int kh = 0; kh < 2; ++kh) {
+        const bf16x8 a =
+            *reinterpret_cast<const bf16x8*>(kbase + kh * 16 * C::ROWB + k_lane + 1024 * ks);
+#pragma unroll
+        for (int qh = 0; qh < kQH; ++qh)
+          s[kh][qh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qreg[qh][ks],
+                                                              ks == 0 ? f32x4{} : s[kh][qh], 0, 0, 0);
+      }
+    // all K reads first, then the products
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::KS, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * C::KS, 0);
   };
-  // mask keys >= n_valid of a 32-key block (register j holds key 8 (j / 4) + 4 half + j % 4)
-  auto mask_blk = [&](f32x16 (&s)[kCB], int n_valid) __attribute__((always_inline)) {
+  // mask keys >= n_valid of a 32-key block
+  auto mask_blk = [&](f32x4 (&s)[2][kQH], int n_valid) __attribute__((always_inline)) {
 #pragma unroll
-    for (int cb = 0; cb < kCB; ++cb)
+    for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-      for (int j = 0; j < 16; ++j)
-        s[cb][j] = 8 * (j >> 2) + 4 * half + (j & 3) >= n_valid ? -INFINITY : s[cb][j];
+      for (int qh = 0; qh < kQH; ++qh)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          s[kh][qh][j] = 4 * grp >= n_valid - 16 * kh - j ? -INFINITY : s[kh][qh][j];
+  };
+  // column max of a block for query half qh (every lane of the query agrees)
+  auto col_max = [&](const f32x4 (&s)[2][kQH], int qh) __attribute__((always_inline)) {
+    float mx = fmaxf(fmaxf(s[0][qh][0], s[0][qh][1]), fmaxf(s[0][qh][2], s[0][qh][3]));
+    mx = fmaxf(mx, fmaxf(fmaxf(s[1][qh][0], s[1][qh][1]), fmaxf(s[1][qh][2], s[1][qh][3])));
+    return max_across_groups(mx);
   };
   // reference max from the first block: its column max (O and l are still zero)
-  auto first_max = [&](const f32x16 (&s)[kCB]) __attribute__((always_inline)) {
+  auto first_max = [&](const f32x4 (&s)[2][kQH]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int cb = 0; cb < kCB; ++cb) {
-      float mx = s[cb][0];
-#pragma unroll
-      for (int j = 1; j < 16; ++j) mx = fmaxf(mx, s[cb][j]);
-      m_run[cb] = max_across_halves(mx) * scale_log2;
-    }
+    for (int qh = 0; qh < kQH; ++qh) m_run[qh] = col_max(s, qh) * scale_log2;
   };
-  // probabilities of a block as packed bf16
-  auto p_blk = [&](const f32x16 (&s)[kCB], uint32_t (&pk)[kCB][8], float (&lb)[kCB])
+  // probabilities of a block as packed bf16: pk[qh] is the P^T operand of query
+  // half qh, keys 4 grp .. 4 grp+3 then 16 + 4 grp .. +3
+  auto p_blk = [&](const f32x4 (&s)[2][kQH], uint32_t (&pk)[kQH][4], float (&lb)[kQH])
       __attribute__((always_inline)) {
 #pragma unroll
-    for (int cb = 0; cb < kCB; ++cb) {
+    for (int qh = 0; qh < kQH; ++qh) {
       float sum = -0.0f;
 #pragma unroll
-      for (int j = 0; j < 16; j += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[cb][j], scale_log2, -m_run[cb]));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[cb][j + 1], scale_log2, -m_run[cb]));
-        sum += p0 + p1;
-        pk[cb][j >> 1] = pack_bf16(p0, p1);
-      }
-      lb[cb] = sum;
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int j = 0; j < 4; j += 2) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kh][qh][j], scale_log2, -m_run[qh]));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kh][qh][j + 1], scale_log2, -m_run[qh]));
+          sum += p0 + p1;
+          pk[qh][2 * kh + (j >> 1)] = pack_bf16(p0, p1);
+        }
+      lb[qh] = sum;
     }
   };
   // The reference max is only raised when a block's probabilities (relative to
@@ -389,56 +412,56 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   // reference raised to its column max (O and l follow) and its probabilities
   // redone.  Below the limit every probability is at most kSumLimit, so nothing
   // overflows; infinities (scores far above the reference) also exceed it.
-  auto check_blk = [&](const char* kt, int kb, int nv_blk, uint32_t (&pk)[kCB][8], float (&lb)[kCB])
+  auto check_blk = [&](const char* kt, int kb, int nv_blk, uint32_t (&pk)[kQH][4], float (&lb)[kQH])
       __attribute__((always_inline)) {
     bool over = false;
 #pragma unroll
-    for (int cb = 0; cb < kCB; ++cb) over |= lb[cb] > kSumLimit;
-    if (__builtin_amdgcn_ballot_w64(over) == 0) return;
-    f32x16 sr[kCB];
-    s_blk(kt, kb, sr);
-    if (nv_blk < 32) mask_blk(sr, nv_blk);
+    for (int qh = 0; qh < kQH; ++qh) over |= lb[qh] > kSumLimit;
+    float alpha[kQH];
 #pragma unroll
-    for (int cb = 0; cb < kCB; ++cb) {
-      float mx = sr[cb][0];
+    for (int qh = 0; qh < kQH; ++qh) alpha[qh] = 1.0f;
+    if (__builtin_amdgcn_ballot_w64(over) != 0) {
+      f32x4 sr[2][kQH];
+      s_blk(kt, kb, sr);
+      if (nv_blk < 32) mask_blk(sr, nv_blk);
 #pragma unroll
-      for (int j = 1; j < 16; ++j) mx = fmaxf(mx, sr[cb][j]);
-      const float m_new = fmaxf(m_run[cb], max_across_halves(mx) * scale_log2);
-      const float alpha = __builtin_amdgcn_exp2f(m_run[cb] - m_new);
-      l_run[cb] *= alpha;
-#pragma unroll
-      for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) o[cb][db][j] *= alpha;
-      m_run[cb] = m_new;
+      for (int qh = 0; qh < kQH; ++qh) {
+        const float m_new = fmaxf(m_run[qh], col_max(sr, qh) * scale_log2);
+        alpha[qh] = __builtin_amdgcn_exp2f(m_run[qh] - m_new);
+        l_run[qh] *= alpha[qh];
+        m_run[qh] = m_new;
+      }
+      p_blk(sr, pk, lb);
     }
-    p_blk(sr, pk, lb);
+    // O follows the raised reference only in the lanes whose reference moved
+    // (a per-lane branch, so the accumulators are scaled where they live)
+    if (alpha[0] != 1.0f || alpha[1] != 1.0f)
+#pragma unroll
+      for (int qh = 0; qh < kQH; ++qh)
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[dt][qh][j] *= alpha[qh];
   };
   // O^T += V^T P^T for 32-key block kb of the tile at vt
-  auto pv_blk = [&](const char* vt, int kb, const uint32_t (&pk)[kCB][8]) __attribute__((always_inline)) {
+  auto pv_blk = [&](const char* vt, int kb, const uint32_t (&pk)[kQH][4]) __attribute__((always_inline)) {
+    bf16x8 pb[kQH];
 #pragma unroll
-    for (int mh = 0; mh < 2; ++mh) {
-      bf16x8 pb[kCB];
+    for (int qh = 0; qh < kQH; ++qh) {
+      const u32x4 pu = {pk[qh][0], pk[qh][1], pk[qh][2], pk[qh][3]};
+      pb[qh] = __builtin_bit_cast(bf16x8, pu);
+    }
+    const char* vbase = vt + kb * 32 * C::ROWB;
 #pragma unroll
-      for (int cb = 0; cb < kCB; ++cb) {
-        const u32x4 pu = {pk[cb][4 * mh + 0], pk[cb][4 * mh + 1], pk[cb][4 * mh + 2],
-                          pk[cb][4 * mh + 3]};
-        pb[cb] = __builtin_bit_cast(bf16x8, pu);
-      }
-      const char* vbase = vt + (kb * 32 + 16 * mh) * C::ROWB;
+    for (int dt = 0; dt < C::DT; ++dt) {
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, vbase + v_lane[0] + 256 * dt));
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, vbase + v_lane[1] + 256 * dt));
+      const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
+      const u32x4 au = {lo2[0], lo2[1], hi2[0], hi2[1]};
+      const bf16x8 a = __builtin_bit_cast(bf16x8, au);
 #pragma unroll
-      for (int db = 0; db < C::DB; ++db) {
-        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            LDS_PTR(s16x4, vbase + (v_lane[0] ^ (db << kVdbShift))));
-        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            LDS_PTR(s16x4, vbase + (v_lane[1] ^ (db << kVdbShift))));
-        const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
-        const u32x4 au = {lo2[0], lo2[1], hi2[0], hi2[1]};
-        const bf16x8 a = __builtin_bit_cast(bf16x8, au);
-#pragma unroll
-        for (int cb = 0; cb < kCB; ++cb)
-          o[cb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[cb], o[cb][db], 0, 0, 0);
-      }
+      for (int qh = 0; qh < kQH; ++qh)
+        o[dt][qh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qh], o[dt][qh], 0, 0, 0);
     }
   };
 
@@ -446,35 +469,35 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   Cursor c_s = {0, 0};                       // the tile of the S^T block being computed
   for (int i = 0; i < t_begin; ++i) c_s = advance(c_s);
   Cursor c_dma = advance(c_s);               // the tile the next copy fetches
-  issue_tile(lds0, c_s);
+  issue_tile(slot(0), c_s);
   if (n_tiles > 1) {
-    issue_tile(lds1, c_dma);
+    issue_tile(slot(1), c_dma);
     c_dma = advance(c_dma);                  // tile 2
   }
   if (n_tiles > 2) {
-    issue_tile(lds2, c_dma);
+    issue_tile(slot(2), c_dma);
     c_dma = advance(c_dma);                  // tile 3
   }
   // S^T of even blocks (block 0 of a tile) lives in s_a, of odd blocks in s_b
-  f32x16 s_a[kCB], s_b[kCB];
-  uint32_t pk[kCB][8];
-  float lb[kCB];
+  f32x4 s_a[2][kQH], s_b[2][kQH];
+  uint32_t pk[kQH][4];
+  float lb[kQH];
   int nv_s = min(kBK, seg_len(c_s.sg) - c_s.k0);   // valid keys of tile c_s
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  s_blk(lds0, 0, s_a);
+  s_blk(slot(0), 0, s_a);
   if (nv_s < 32) mask_blk(s_a, nv_s);
   first_max(s_a);
 
   // ---- main loop over 32-key blocks -------------------------------------------
   // Block b = 2t + kb is key block kb of tile t.  Phase A(b): S^T of block b+1
   // on the matrix core beside the exponentials of block b.  Phase B(b): O^T +=
-  // block b beside the mask and column max of block b+1.  Waves 0-3 run
-  // [barrier t, copy of tile t+2, A(2t) B(2t) A(2t+1) B(2t+1)]; waves 4-7, which
-  // share their SIMDs, run one phase later, [barrier t, B(2t-1) A(2t) B(2t)
-  // A(2t+1)], so each SIMD pairs one wave's exponentials with the other's
-  // products.  Tile t lives in slot t % 4; the last read of tile t (waves 4-7,
-  // B(2t+1)) precedes barrier t+2, where waves 0-3 copy tile t+4 into its slot.
+  // block b beside the mask of block b+1.  Waves 0-3 run [barrier t, A(2t)
+  // B(2t) A(2t+1) B(2t+1), copy of tile t+3]; waves 4-7, which share their
+  // SIMDs, run one phase later, [barrier t, B(2t-1) A(2t) B(2t) A(2t+1)], so
+  // each SIMD pairs one wave's exponentials with the other's products.  Tile t
+  // lives in slot t % 5; the last read of tile t (waves 4-7, B(2t+1)) precedes
+  // barrier t+2, after which waves 0-3 copy tile t+5 into its slot.
   // A(2t):   s_b = S^T(tile t, block 1);   P of s_a.
   // A(2t+1): s_a = S^T(tile t+1, block 0); P of s_b (only P for the last tile).
   auto phA0 = [&](char* st) __attribute__((always_inline)) {
@@ -486,7 +509,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
     check_blk(st, 0, nv_s, pk, lb);
 #pragma unroll
-    for (int cb = 0; cb < kCB; ++cb) l_run[cb] += lb[cb];
+    for (int qh = 0; qh < kQH; ++qh) l_run[qh] += lb[qh];
     pv_blk(st + C::TILE, 0, pk);
     if (nv_s < kBK) mask_blk(s_b, nv_s - 32);
   };
@@ -499,7 +522,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
     check_blk(st, 1, nv_s - 32, pk, lb);
 #pragma unroll
-    for (int cb = 0; cb < kCB; ++cb) l_run[cb] += lb[cb];
+    for (int qh = 0; qh < kQH; ++qh) l_run[qh] += lb[qh];
     pv_blk(st + C::TILE, 1, pk);
     if (t + 1 < n_tiles) {
       c_s = advance(c_s);
@@ -530,17 +553,13 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
         c_dma = advance(c_dma);
       }
     };
-    for (int t = 0; t < n_tiles;) {
-      step(t, lds0, lds1, lds3);
-      if (++t >= n_tiles) break;
-      step(t, lds1, lds2, lds4);
-      if (++t >= n_tiles) break;
-      step(t, lds2, lds3, lds0);
-      if (++t >= n_tiles) break;
-      step(t, lds3, lds4, lds1);
-      if (++t >= n_tiles) break;
-      step(t, lds4, lds0, lds2);
-      ++t;
+    int i0 = 0;   // slot of tile t
+#pragma unroll 1
+    for (int t = 0; t < n_tiles; ++t) {
+      const int i1 = i0 == 4 ? 0 : i0 + 1;
+      const int i3 = i0 >= 2 ? i0 - 2 : i0 + 3;
+      step(t, slot(i0), slot(i1), slot(i3));
+      i0 = i1;
     }
     sync(n_tiles);   // matches the extra barrier of the last step of waves 4-7
   } else {
@@ -555,60 +574,51 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
         phA1(t, s1);
       }
     };
-    for (int t = 0;;) {
-      step(t, lds4, lds0, lds1);
-      if (t++ >= n_tiles) break;
-      step(t, lds0, lds1, lds2);
-      if (t++ >= n_tiles) break;
-      step(t, lds1, lds2, lds3);
-      if (t++ >= n_tiles) break;
-      step(t, lds2, lds3, lds4);
-      if (t++ >= n_tiles) break;
-      step(t, lds3, lds4, lds0);
-      if (t++ >= n_tiles) break;
+    int i0 = 0;   // slot of tile t
+#pragma unroll 1
+    for (int t = 0;; ++t) {
+      const int ip = i0 == 0 ? 4 : i0 - 1;
+      const int i1 = i0 == 4 ? 0 : i0 + 1;
+      step(t, slot(ip), slot(i0), slot(i1));
+      if (t >= n_tiles) break;
+      i0 = i1;
     }
   }
 
-  // normalise and store: register j of block db holds d = 32 db + 8 (j / 4) + 4 half + j % 4
+  // normalise and store: lane (l16, grp) of tile (dt, qh) holds query
+  // q0 + 16 qh + l16 at d = 16 dt + 4 grp + j
 #pragma unroll
-  for (int cb = 0; cb < kCB; ++cb) {
-    const int qi = q0 + 32 * cb + l32;
-    const float l_tot = sum_across_halves(l_run[cb]);
+  for (int qh = 0; qh < kQH; ++qh) {
+    const int qi = q0 + 16 * qh + l16;
+    const float l_tot = sum_across_groups(l_run[qh]);
     const float inv = 1.0f / l_tot;
     if constexpr (kPacked) {
       // base-2 log-sum-exp of the scaled logits, for the backward pass
-      if (src.lse != nullptr && half == 0 && qi < nq)
-        src.lse[(int64_t(chunk) * nq + qi) * heads + head] = m_run[cb] + log2f(l_tot);
+      if (src.lse != nullptr && grp == 0 && qi < nq)
+        src.lse[(int64_t(chunk) * nq + qi) * heads + head] = m_run[qh] + log2f(l_tot);
     }
     if (n_parts > 1) {
       // unnormalised partial result of this part: O (row = query of the
       // workgroup), the reference max and the sum, merged by the tail kernel
       float* pb = tail.part + size_t((logical - tail.n_full) * n_parts + part_id) *
                                   (kBlockQ * D + 2 * kBlockQ);
-      const int row = wave * kWaveQ + 32 * cb + l32;
+      const int row = wave * kWaveQ + 16 * qh + l16;
 #pragma unroll
-      for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          const f32x4 v = {o[cb][db][4 * a + 0], o[cb][db][4 * a + 1], o[cb][db][4 * a + 2],
-                           o[cb][db][4 * a + 3]};
-          *reinterpret_cast<f32x4*>(pb + row * D + 32 * db + 8 * a + 4 * half) = v;
-        }
-      if (half == 0) {
-        pb[kBlockQ * D + row] = m_run[cb];
+      for (int dt = 0; dt < C::DT; ++dt)
+        *reinterpret_cast<f32x4*>(pb + row * D + 16 * dt + 4 * grp) = o[dt][qh];
+      if (grp == 0) {
+        pb[kBlockQ * D + row] = m_run[qh];
         pb[kBlockQ * D + kBlockQ + row] = l_tot;
       }
     } else if (qi < nq) {
-      __bf16* op = out + (int64_t(qi) * heads + head) * D + 4 * half;
+      __bf16* op = out + (int64_t(qi) * heads + head) * D + 4 * grp;
 #pragma unroll
-      for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          u32x2 w;
-          w.x = pack_bf16(o[cb][db][4 * a + 0] * inv, o[cb][db][4 * a + 1] * inv);
-          w.y = pack_bf16(o[cb][db][4 * a + 2] * inv, o[cb][db][4 * a + 3] * inv);
-          *reinterpret_cast<u32x2*>(op + 32 * db + 8 * a) = w;
-        }
+      for (int dt = 0; dt < C::DT; ++dt) {
+        u32x2 w;
+        w.x = pack_bf16(o[dt][qh][0] * inv, o[dt][qh][1] * inv);
+        w.y = pack_bf16(o[dt][qh][2] * inv, o[dt][qh][3] * inv);
+        *reinterpret_cast<u32x2*>(op + 16 * dt) = w;
+      }
     }
   }
 }
