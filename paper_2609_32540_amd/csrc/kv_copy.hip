@@ -8,7 +8,9 @@
 // 16-byte vectors; a block moves kTokensPerBlock consecutive tokens of one
 // head, so the head-major side is one contiguous run and the token-major side
 // is rows of row_bytes at a stride of heads * row_bytes.  Each thread issues
-// all of its loads before its stores to keep several 16-byte loads in flight.
+// all of its loads before its stores to keep several 16-byte loads in flight;
+// blocks whose tokens are all in range do so without per-lane checks (checked
+// loads would each be waited for before the next).
 
 #include <hip/hip_runtime.h>
 
@@ -36,24 +38,31 @@ __global__ __launch_bounds__(kThreads) void kv_copy_kernel(
   const int r = threadIdx.x / VPR;
   const int tok0 = blockIdx.x * kTokensPerBlock + r;
 
+  auto index = [&](int t, bool to_head_major) {
+    return to_head_major ? head * head_stride_vec + int64_t(t) * VPR + c     // head-major index
+                         : (int64_t(t) * heads + head) * VPR + c;            // token-major index
+  };
   u32x4 val[ITER];
+  if ((blockIdx.x + 1) * kTokensPerBlock <= n_tok) {
+    // a whole block of tokens: no per-lane check, so every load is in flight
+    // before the first store
 #pragma unroll
-  for (int it = 0; it < ITER; ++it) {
-    const int t = tok0 + it * kRowsPerPass;
-    if (t < n_tok) {
-      const int64_t tm = (int64_t(t) * heads + head) * VPR + c;   // token-major index
-      const int64_t hm = head * head_stride_vec + int64_t(t) * VPR + c;  // head-major index
-      val[it] = __builtin_nontemporal_load(src + (kToHeadMajor ? tm : hm));
-    }
+    for (int it = 0; it < ITER; ++it)
+      val[it] = __builtin_nontemporal_load(src + index(tok0 + it * kRowsPerPass, !kToHeadMajor));
+#pragma unroll
+    for (int it = 0; it < ITER; ++it)
+      __builtin_nontemporal_store(val[it], dst + index(tok0 + it * kRowsPerPass, kToHeadMajor));
+    return;
   }
 #pragma unroll
   for (int it = 0; it < ITER; ++it) {
     const int t = tok0 + it * kRowsPerPass;
-    if (t < n_tok) {
-      const int64_t tm = (int64_t(t) * heads + head) * VPR + c;
-      const int64_t hm = head * head_stride_vec + int64_t(t) * VPR + c;
-      __builtin_nontemporal_store(val[it], dst + (kToHeadMajor ? hm : tm));
-    }
+    if (t < n_tok) val[it] = __builtin_nontemporal_load(src + index(t, !kToHeadMajor));
+  }
+#pragma unroll
+  for (int it = 0; it < ITER; ++it) {
+    const int t = tok0 + it * kRowsPerPass;
+    if (t < n_tok) __builtin_nontemporal_store(val[it], dst + index(t, kToHeadMajor));
   }
 }
 
