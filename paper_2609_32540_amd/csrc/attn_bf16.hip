@@ -65,6 +65,8 @@
 
 #include <math.h>
 
+#include <utility>
+
 #include "ff_internal.h"
 
 namespace ff {
@@ -79,6 +81,7 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
 #define GLOBAL_PTR(p) ((const __attribute__((address_space(1))) void*)(p))
 
@@ -89,7 +92,9 @@ constexpr int kWaveQ = 16 * kQH;            // queries per wave
 constexpr int kBlockQ = kWaves * kWaveQ;    // queries per workgroup
 constexpr int kBK = 64;                     // keys per tile
 constexpr int kXcds = 8;
-constexpr float kSumLimit = 16.0f;          // largest block sum of probabilities kept
+constexpr float kSumLimit = 16.0f;          // checked pass: largest block sum of probabilities kept
+constexpr float kFastLimit = 256.0f;        // fast pass: largest block sum before the checked pass
+constexpr int kHalfVALU = 20;               // plain VALU of a query half: 8 fma + 8 add + 4 packs
 // Waves w and w + 4 share a SIMD and the issue arbiter favours the older one
 // (w < 4), which reaches each tile's barrier well ahead of its partner; the
 // tile copies are therefore all issued by waves 0-3, off the partner's path.
@@ -148,6 +153,39 @@ __device__ inline uint64_t readlane_u64(uint64_t v, int lane) {
   const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), lane));
   const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v >> 32)), lane));
   return (uint64_t(hi) << 32) | uint64_t(lo);
+}
+
+// s_waitcnt immediate: vmcnt = vm; lgkmcnt and expcnt not waited for
+constexpr int waitcnt_vm(int vm) { return (vm & 15) | ((vm >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// Instruction order of one half of a pipeline step, by sched_group_barrier
+// classes (0x008 matrix, 0x100 LDS read, 0x002 VALU, 0x400 transcendental):
+// NM products, each followed by its share of the half's NR LDS reads and of
+// the softmax of one query half (NV plain VALU instructions: 8 fma, 8 add, 4
+// packs and some slack; 8 exponentials), a few softmax instructions ahead of
+// the first product.
+template <int NM, int NR, int NV, int NT, int I>
+__device__ __forceinline__ void interleave_one() {
+  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  constexpr int r = (NR * (I + 1)) / NM - (NR * I) / NM;
+  if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);
+  constexpr int v = (NV * (I + 1)) / NM - (NV * I) / NM;
+  if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x002, v, 0);
+  constexpr int t = (NT * (I + 1)) / NM - (NT * I) / NM;
+  if constexpr (t > 0) __builtin_amdgcn_sched_group_barrier(0x400, t, 0);
+}
+
+template <int NM, int NR, int NV, int NT, int... I>
+__device__ __forceinline__ void interleave_seq(std::integer_sequence<int, I...>) {
+  (interleave_one<NM, NR, NV, NT, I>(), ...);
+}
+
+template <int NM, int NR, int NV>
+__device__ __forceinline__ void interleave_half() {
+  constexpr int kHead = 2, kHeadT = 1;
+  __builtin_amdgcn_sched_group_barrier(0x002, kHead, 0);
+  __builtin_amdgcn_sched_group_barrier(0x400, kHeadT, 0);
+  interleave_seq<NM, NR, NV - kHead, 8 - kHeadT>(std::make_integer_sequence<int, NM>{});
 }
 
 // Tile cursor over the key segments: tile = (segment, first key).
@@ -347,25 +385,54 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     v_lane[hi] = (r >> 3) * (8 * C::ROWB) + ((2 * (r & 7) + ((l16 >> 1) & 1)) << 4) + 8 * (l16 & 1);
   }
 
-  // S^T of 32-key block kb of the tile at kt: tile (kh, qh) = keys 16 kh .. +15 x
-  // queries 16 qh .. +15 of the wave; lane (l16, grp) register j holds key
-  // 16 kh + 4 grp + j of query 16 qh + l16
-  auto s_blk = [&](const char* kt, int kb, f32x4 (&s)[2][kQH]) __attribute__((always_inline)) {
+  // K operands of S^T for 32-key block kb of the tile at kt: a[kh][ks] = rows
+  // 16 kh + l16, d slice ks
+  auto k_read = [&](const char* kt, int kb, bf16x8 (&a)[2][C::KS]) __attribute__((always_inline)) {
     const char* kbase = kt + kb * 32 * C::ROWB;
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks)
+        a[kh][ks] = *reinterpret_cast<const bf16x8*>(kbase + kh * 16 * C::ROWB + k_lane + 1024 * ks);
+  };
+  // S^T of a block: tile (kh, qh) = keys 16 kh .. +15 x queries 16 qh .. +15 of
+  // the wave; lane (l16, grp) register j holds key 16 kh + 4 grp + j of query
+  // 16 qh + l16
+  auto s_mma = [&](const bf16x8 (&a)[2][C::KS], f32x4 (&s)[2][kQH]) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks)
 #pragma unroll
-      for (int kh = 0; kh < 2; ++kh) {
-        const bf16x8 a =
-            *reinterpret_cast<const bf16x8*>(kbase + kh * 16 * C::ROWB + k_lane + 1024 * ks);
+      for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
         for (int qh = 0; qh < kQH; ++qh)
-          s[kh][qh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qreg[qh][ks],
+          s[kh][qh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kh][ks], qreg[qh][ks],
                                                               ks == 0 ? f32x4{} : s[kh][qh], 0, 0, 0);
-      }
-    // all K reads first, then the products
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::KS, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 4 * C::KS, 0);
+  };
+  // V^T operands of O^T for 32-key block kb of the tile at vt, d tile dt
+  auto v_read = [&](const char* vt, int kb, bf16x8 (&a)[C::DT]) __attribute__((always_inline)) {
+    const char* vbase = vt + kb * 32 * C::ROWB;
+#pragma unroll
+    for (int dt = 0; dt < C::DT; ++dt) {
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, vbase + v_lane[0] + 256 * dt));
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, vbase + v_lane[1] + 256 * dt));
+      const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
+      const u32x4 au = {lo2[0], lo2[1], hi2[0], hi2[1]};
+      a[dt] = __builtin_bit_cast(bf16x8, au);
+    }
+  };
+  // O^T += V^T P^T for one block
+  auto pv_mma = [&](const bf16x8 (&a)[C::DT], const uint32_t (&pk)[kQH][4]) __attribute__((always_inline)) {
+    bf16x8 pb[kQH];
+#pragma unroll
+    for (int qh = 0; qh < kQH; ++qh) {
+      const u32x4 pu = {pk[qh][0], pk[qh][1], pk[qh][2], pk[qh][3]};
+      pb[qh] = __builtin_bit_cast(bf16x8, pu);
+    }
+#pragma unroll
+    for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+      for (int qh = 0; qh < kQH; ++qh)
+        o[dt][qh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[dt], pb[qh], o[dt][qh], 0, 0, 0);
   };
   // mask keys >= n_valid of a 32-key block
   auto mask_blk = [&](f32x4 (&s)[2][kQH], int n_valid) __attribute__((always_inline)) {
@@ -383,205 +450,228 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     mx = fmaxf(mx, fmaxf(fmaxf(s[1][qh][0], s[1][qh][1]), fmaxf(s[1][qh][2], s[1][qh][3])));
     return max_across_groups(mx);
   };
-  // reference max from the first block: its column max (O and l are still zero)
-  auto first_max = [&](const f32x4 (&s)[2][kQH]) __attribute__((always_inline)) {
+  // probabilities of query half qh of a block as packed bf16: pk[qh] is the
+  // P^T operand of that half, keys 4 grp .. 4 grp+3 then 16 + 4 grp .. +3; lb[qh]
+  // is this lane's share of the block's row sum
+  auto p_half = [&](const f32x4 (&s)[2][kQH], int qh, uint32_t (&pk)[kQH][4], float (&lb)[kQH])
+      __attribute__((always_inline)) {
+    float sum = 0.0f;
 #pragma unroll
-    for (int qh = 0; qh < kQH; ++qh) m_run[qh] = col_max(s, qh) * scale_log2;
+    for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+      for (int j = 0; j < 4; j += 2) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kh][qh][j], scale_log2, -m_run[qh]));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kh][qh][j + 1], scale_log2, -m_run[qh]));
+        const uint32_t w = pack_bf16(p0, p1);
+        pk[qh][2 * kh + (j >> 1)] = w;
+        sum += p0 + p1;
+      }
+    lb[qh] = sum;
   };
-  // probabilities of a block as packed bf16: pk[qh] is the P^T operand of query
-  // half qh, keys 4 grp .. 4 grp+3 then 16 + 4 grp .. +3
   auto p_blk = [&](const f32x4 (&s)[2][kQH], uint32_t (&pk)[kQH][4], float (&lb)[kQH])
       __attribute__((always_inline)) {
 #pragma unroll
-    for (int qh = 0; qh < kQH; ++qh) {
-      float sum = -0.0f;
-#pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-        for (int j = 0; j < 4; j += 2) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kh][qh][j], scale_log2, -m_run[qh]));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kh][qh][j + 1], scale_log2, -m_run[qh]));
-          sum += p0 + p1;
-          pk[qh][2 * kh + (j >> 1)] = pack_bf16(p0, p1);
-        }
-      lb[qh] = sum;
-    }
+    for (int qh = 0; qh < kQH; ++qh) p_half(s, qh, pk, lb);
   };
   // The reference max is only raised when a block's probabilities (relative to
-  // it) sum past kSumLimit: then this block's S^T is recomputed from LDS, the
-  // reference raised to its column max (O and l follow) and its probabilities
-  // redone.  Below the limit every probability is at most kSumLimit, so nothing
-  // overflows; infinities (scores far above the reference) also exceed it.
-  auto check_blk = [&](const char* kt, int kb, int nv_blk, uint32_t (&pk)[kQH][4], float (&lb)[kQH])
+  // it) sum past kSumLimit: then the reference is raised to the block's column
+  // max (O and l follow) and its probabilities are redone from the scores, which
+  // are still in registers.  Below the limit every probability is at most
+  // kSumLimit, so nothing overflows; infinities (scores far above the
+  // reference) also exceed it.  O is rescaled after the products of the previous
+  // block (issued in the same step) have been added into it.
+  auto check_blk = [&](const f32x4 (&s)[2][kQH], uint32_t (&pk)[kQH][4], float (&lb)[kQH])
       __attribute__((always_inline)) {
     bool over = false;
 #pragma unroll
     for (int qh = 0; qh < kQH; ++qh) over |= lb[qh] > kSumLimit;
-    float alpha[kQH];
-#pragma unroll
-    for (int qh = 0; qh < kQH; ++qh) alpha[qh] = 1.0f;
     if (__builtin_amdgcn_ballot_w64(over) != 0) {
-      f32x4 sr[2][kQH];
-      s_blk(kt, kb, sr);
-      if (nv_blk < 32) mask_blk(sr, nv_blk);
+      float alpha[kQH];
 #pragma unroll
       for (int qh = 0; qh < kQH; ++qh) {
-        const float m_new = fmaxf(m_run[qh], col_max(sr, qh) * scale_log2);
+        const float m_new = fmaxf(m_run[qh], col_max(s, qh) * scale_log2);
         alpha[qh] = __builtin_amdgcn_exp2f(m_run[qh] - m_new);
         l_run[qh] *= alpha[qh];
         m_run[qh] = m_new;
       }
-      p_blk(sr, pk, lb);
+      p_blk(s, pk, lb);
+      // O follows the raised reference only in the lanes whose reference moved
+      if (alpha[0] != 1.0f || alpha[1] != 1.0f)
+#pragma unroll
+        for (int qh = 0; qh < kQH; ++qh)
+#pragma unroll
+          for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) o[dt][qh][j] *= alpha[qh];
     }
-    // O follows the raised reference only in the lanes whose reference moved
-    // (a per-lane branch, so the accumulators are scaled where they live)
-    if (alpha[0] != 1.0f || alpha[1] != 1.0f)
-#pragma unroll
-      for (int qh = 0; qh < kQH; ++qh)
-#pragma unroll
-        for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) o[dt][qh][j] *= alpha[qh];
-  };
-  // O^T += V^T P^T for 32-key block kb of the tile at vt
-  auto pv_blk = [&](const char* vt, int kb, const uint32_t (&pk)[kQH][4]) __attribute__((always_inline)) {
-    bf16x8 pb[kQH];
-#pragma unroll
-    for (int qh = 0; qh < kQH; ++qh) {
-      const u32x4 pu = {pk[qh][0], pk[qh][1], pk[qh][2], pk[qh][3]};
-      pb[qh] = __builtin_bit_cast(bf16x8, pu);
-    }
-    const char* vbase = vt + kb * 32 * C::ROWB;
-#pragma unroll
-    for (int dt = 0; dt < C::DT; ++dt) {
-      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, vbase + v_lane[0] + 256 * dt));
-      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, vbase + v_lane[1] + 256 * dt));
-      const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
-      const u32x4 au = {lo2[0], lo2[1], hi2[0], hi2[1]};
-      const bf16x8 a = __builtin_bit_cast(bf16x8, au);
-#pragma unroll
-      for (int qh = 0; qh < kQH; ++qh)
-        o[dt][qh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[qh], o[dt][qh], 0, 0, 0);
-    }
-  };
-
-  // ---- prologue: tiles 0 and 1 in flight, S^T of block 0 of tile 0 ----------------
-  Cursor c_s = {0, 0};                       // the tile of the S^T block being computed
-  for (int i = 0; i < t_begin; ++i) c_s = advance(c_s);
-  Cursor c_dma = advance(c_s);               // the tile the next copy fetches
-  issue_tile(slot(0), c_s);
-  if (n_tiles > 1) {
-    issue_tile(slot(1), c_dma);
-    c_dma = advance(c_dma);                  // tile 2
-  }
-  if (n_tiles > 2) {
-    issue_tile(slot(2), c_dma);
-    c_dma = advance(c_dma);                  // tile 3
-  }
-  // S^T of even blocks (block 0 of a tile) lives in s_a, of odd blocks in s_b
-  f32x4 s_a[2][kQH], s_b[2][kQH];
-  uint32_t pk[kQH][4];
-  float lb[kQH];
-  int nv_s = min(kBK, seg_len(c_s.sg) - c_s.k0);   // valid keys of tile c_s
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  s_blk(slot(0), 0, s_a);
-  if (nv_s < 32) mask_blk(s_a, nv_s);
-  first_max(s_a);
-
-  // ---- main loop over 32-key blocks -------------------------------------------
-  // Block b = 2t + kb is key block kb of tile t.  Phase A(b): S^T of block b+1
-  // on the matrix core beside the exponentials of block b.  Phase B(b): O^T +=
-  // block b beside the mask of block b+1.  Waves 0-3 run [barrier t, A(2t)
-  // B(2t) A(2t+1) B(2t+1), copy of tile t+3]; waves 4-7, which share their
-  // SIMDs, run one phase later, [barrier t, B(2t-1) A(2t) B(2t) A(2t+1)], so
-  // each SIMD pairs one wave's exponentials with the other's products.  Tile t
-  // lives in slot t % 5; the last read of tile t (waves 4-7, B(2t+1)) precedes
-  // barrier t+2, after which waves 0-3 copy tile t+5 into its slot.
-  // A(2t):   s_b = S^T(tile t, block 1);   P of s_a.
-  // A(2t+1): s_a = S^T(tile t+1, block 0); P of s_b (only P for the last tile).
-  auto phA0 = [&](char* st) __attribute__((always_inline)) {
-    asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
-    s_blk(st, 1, s_b);
-    p_blk(s_a, pk, lb);
-  };
-  auto phB0 = [&](char* st) __attribute__((always_inline)) {
-    asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
-    check_blk(st, 0, nv_s, pk, lb);
 #pragma unroll
     for (int qh = 0; qh < kQH; ++qh) l_run[qh] += lb[qh];
-    pv_blk(st + C::TILE, 0, pk);
-    if (nv_s < kBK) mask_blk(s_b, nv_s - 32);
   };
-  auto phA1 = [&](int t, char* sn) __attribute__((always_inline)) {
-    asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
-    s_blk(sn, 0, s_a);   // (after the last tile: stale slot, result unused)
-    p_blk(s_b, pk, lb);
+  // One step of the block pipeline, in two halves that the scheduler may not
+  // mix: (1) the V reads of this step, S^T of block b+1 from the K operands read
+  // in the previous step and the softmax of query half 0 of block b; (2) the K
+  // reads of the next step (tile kt_next, key block kb_next, into the registers
+  // the S^T products have just consumed), O^T += P(b-1) V(b-1) and the softmax
+  // of query half 1.  Inside a half every product is followed by its share of
+  // the LDS reads and of the softmax work (exponentials, row sums, bf16
+  // packing), which depends on no product of the step.
+  auto step = [&](bf16x8 (&ka)[2][C::KS], const char* vt, int kbv, const char* kt_next, int kb_next,
+                  const f32x4 (&s_in)[2][kQH], f32x4 (&s_out)[2][kQH],
+                  const uint32_t (&pk_in)[kQH][4], uint32_t (&pk_out)[kQH][4], float (&lb)[kQH])
+      __attribute__((always_inline)) {
+    bf16x8 va[C::DT];
+    v_read(vt, kbv, va);
+    s_mma(ka, s_out);
+    p_half(s_in, 0, pk_out, lb);
+    interleave_half<4 * C::KS, 2 * C::DT, kHalfVALU>();
+    __builtin_amdgcn_sched_barrier(0);
+    k_read(kt_next, kb_next, ka);
+    pv_mma(va, pk_in);
+    p_half(s_in, 1, pk_out, lb);
+    interleave_half<2 * C::DT, 2 * C::KS, kHalfVALU>();
+    // (the softmax results are computed inside this step, not sunk past the
+    // branches that follow it)
+    asm volatile("" ::"v"(pk_out[0][0]), "v"(pk_out[0][1]), "v"(pk_out[0][2]), "v"(pk_out[0][3]),
+                 "v"(pk_out[1][0]), "v"(pk_out[1][1]), "v"(pk_out[1][2]), "v"(pk_out[1][3]),
+                 "v"(lb[0]), "v"(lb[1]));
+    __builtin_amdgcn_sched_barrier(0);
   };
-  auto phB1 = [&](int t, char* st) __attribute__((always_inline)) {
-    asm volatile("" : "+v"(v_lane[0]), "+v"(v_lane[1]));
-    check_blk(st, 1, nv_s - 32, pk, lb);
+
+  // The key loop runs first as a fast pass: the reference max stays the first
+  // block's column max and a block only records whether its probabilities
+  // summed past kFastLimit (no branch).  Below that limit every probability is
+  // at most kFastLimit, nothing overflows, and how far the reference sits below
+  // the true max changes only the scale of O and l, not their ratio.  If any
+  // wave of the workgroup recorded an overflow (scores far above the first
+  // block's, or not finite), the workgroup runs its unit again as a checked
+  // pass, whose reference is raised per block (check_blk); strongly peaked rows
+  // thereby also get the reference at their largest score, where the dominant
+  // probability is exactly 1.
+  bool overflow = false;
+  auto key_loop = [&](auto checked) __attribute__((always_inline)) {
+    constexpr bool kChecked = decltype(checked)::value;
+    auto after_step = [&](const f32x4 (&s)[2][kQH], uint32_t (&pk)[kQH][4], float (&lb)[kQH])
+        __attribute__((always_inline)) {
+      if constexpr (kChecked) {
+        check_blk(s, pk, lb);
+      } else {
 #pragma unroll
-    for (int qh = 0; qh < kQH; ++qh) l_run[qh] += lb[qh];
-    pv_blk(st + C::TILE, 1, pk);
-    if (t + 1 < n_tiles) {
-      c_s = advance(c_s);
-      nv_s = min(kBK, seg_len(c_s.sg) - c_s.k0);
-      if (nv_s < 32) mask_blk(s_a, nv_s);
-    }
-  };
-  // barrier t: tile t+1 has landed (the copy of tile t+2, issued at the end of
-  // step t-1, may still be in flight) and every read of tile t-2 is done
-  auto sync = [&](int t) __attribute__((always_inline)) {
-    if (wave < kCopyWaves && t + 2 < n_tiles)
-      __builtin_amdgcn_s_waitcnt(2 * C::BLOCKS_PER_WAVE);   // vmcnt(copies of one tile), lgkmcnt(0)
-    else
-      __builtin_amdgcn_s_waitcnt(0);
-    asm volatile("s_barrier" ::: "memory");
-  };
-  if (wave < kCopyWaves) {
-    // step t: A(2t) B(2t) A(2t+1) B(2t+1), then the copy of tile t+3 into the
-    // slot of tile t-2 (last read before barrier t)
-    auto step = [&](int t, char* s0, char* s1, char* s3) __attribute__((always_inline)) {
-      sync(t);
-      phA0(s0);
-      phB0(s0);
-      phA1(t, s1);
-      phB1(t, s0);
-      if (t + 3 < n_tiles) {
-        issue_tile(s3, c_dma);
-        c_dma = advance(c_dma);
+        for (int qh = 0; qh < kQH; ++qh) {
+          overflow |= !(lb[qh] <= kFastLimit);   // (a NaN sum counts as an overflow)
+          l_run[qh] += lb[qh];
+        }
       }
     };
+
+    // ---- prologue: tiles 0 .. 2 in flight, S^T of block 0 ----------------------
+    // Tile t lives in slot t % 5.  Block b = 2t + kb is key block kb of tile t.
+    Cursor c_t = {0, 0};                       // tile t of the loop below
+    for (int i = 0; i < t_begin; ++i) c_t = advance(c_t);
+    Cursor c_dma = c_t;                        // the tile the next copy fetches
+#pragma unroll
+    for (int i = 0; i < 3; ++i)
+      if (i < n_tiles) {
+        issue_tile(slot(i), c_dma);
+        c_dma = advance(c_dma);
+      }
+    // S^T of even blocks (block 0 of a tile) lives in s_a, of odd blocks in s_b;
+    // P of even blocks in pk_a, of odd blocks in pk_b
+    f32x4 s_a[2][kQH], s_b[2][kQH];
+    uint32_t pk_a[kQH][4], pk_b[kQH][4];
+    float lb[kQH];
+    bf16x8 ka[2][C::KS];
+    int nv = min(kBK, seg_len(c_t.sg) - c_t.k0);   // valid keys of tile t
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    k_read(slot(0), 0, ka);
+    s_mma(ka, s_a);
+    k_read(slot(0), 1, ka);
+    if (nv < 32) mask_blk(s_a, nv);
+    // reference max from the first block: its column max (O and l are zero)
+#pragma unroll
+    for (int qh = 0; qh < kQH; ++qh) m_run[qh] = col_max(s_a, qh) * scale_log2;
+    // the first step adds P = 0 times V of tile 0 (finite) into O^T
+#pragma unroll
+    for (int qh = 0; qh < kQH; ++qh)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pk_b[qh][i] = 0;
+
+    // ---- main loop over tiles: a barrier and two pipeline steps per tile -----
+    // barrier t: tile t+1 has landed and tile t-2 is no longer read; the waves
+    //            copy tile t+3 into its slot.
+    // A(t): S^T(2t+1) (tile t);   O^T += P(2t-1) V(2t-1) (tile t-1);  P(2t);
+    //       K of tile t+1, block 0.
+    // B(t): S^T(2t+2) (tile t+1); O^T += P(2t) V(2t) (tile t);        P(2t+1);
+    //       K of tile t+1, block 1.
+    // (after the last tile the K reads and S^T products use a stale slot:
+    // result unused)
     int i0 = 0;   // slot of tile t
 #pragma unroll 1
     for (int t = 0; t < n_tiles; ++t) {
       const int i1 = i0 == 4 ? 0 : i0 + 1;
-      const int i3 = i0 >= 2 ? i0 - 2 : i0 + 3;
-      step(t, slot(i0), slot(i1), slot(i3));
+      const int i4 = i0 == 0 ? 4 : i0 - 1;        // slot of tile t-1
+      const int i3 = i0 >= 2 ? i0 - 2 : i0 + 3;   // slot of tile t-2 (and of tile t+3)
+      // each copying wave waits for its own copies of tile t+1 (those of tile
+      // t+2 may stay in flight); LDS reads need no wait: the last reads of tile
+      // t-2 were consumed by products of the previous tile
+      if (wave < kCopyWaves) {
+        if (t + 2 < n_tiles)
+          __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * C::BLOCKS_PER_WAVE));
+        else
+          __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+      }
+      asm volatile("s_barrier" ::: "memory");
+      if (t + 3 < n_tiles) {
+        issue_tile(slot(i3), c_dma);
+        c_dma = advance(c_dma);
+      }
+      char* st = slot(i0);
+      char* sn = slot(i1);
+      step(ka, (t == 0 ? st : slot(i4)) + C::TILE, 1, sn, 0, s_a, s_b, pk_b, pk_a, lb);
+      if (nv < kBK) mask_blk(s_b, nv - 32);   // keys past a segment's end
+      after_step(s_a, pk_a, lb);
+      int nv_next = 32;   // valid keys of tile t+1 (no mask after the last tile)
+      if (t + 1 < n_tiles) {
+        c_t = advance(c_t);
+        nv_next = min(kBK, seg_len(c_t.sg) - c_t.k0);
+      }
+      step(ka, st + C::TILE, 0, sn, 1, s_b, s_a, pk_a, pk_b, lb);
+      if (nv_next < 32) mask_blk(s_a, nv_next);
+      after_step(s_b, pk_b, lb);
+      nv = nv_next;
       i0 = i1;
     }
-    sync(n_tiles);   // matches the extra barrier of the last step of waves 4-7
-  } else {
-    // step t: barrier t, B(2t-1) (t > 0), then A(2t) B(2t) A(2t+1) while
-    // t < n_tiles; the step with t = n_tiles only finishes the last tile.
-    auto step = [&](int t, char* sp, char* s0, char* s1) __attribute__((always_inline)) {
-      sync(t);
-      if (t > 0) phB1(t - 1, sp);
-      if (t < n_tiles) {
-        phA0(s0);
-        phB0(s0);
-        phA1(t, s1);
-      }
-    };
-    int i0 = 0;   // slot of tile t
-#pragma unroll 1
-    for (int t = 0;; ++t) {
-      const int ip = i0 == 0 ? 4 : i0 - 1;
-      const int i1 = i0 == 4 ? 0 : i0 + 1;
-      step(t, slot(ip), slot(i0), slot(i1));
-      if (t >= n_tiles) break;
-      i0 = i1;
+    {
+      // O^T += P(2n-1) V(2n-1): block 1 of the last tile
+      bf16x8 va[C::DT];
+      v_read(slot(i0 == 0 ? 4 : i0 - 1) + C::TILE, 1, va);
+      pv_mma(va, pk_b);
+    }
+  };
+
+  key_loop(std::false_type{});
+  // One flag per wave through LDS (the tiles are no longer read after the
+  // first barrier; the last one keeps the flags from being overwritten by the
+  // checked pass's copies before every wave has read them).
+  {
+    const bool mine = __builtin_amdgcn_ballot_w64(overflow) != 0;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    int* flags = reinterpret_cast<int*>(lds);
+    if (lane == 0) flags[wave] = mine ? 1 : 0;
+    __syncthreads();
+    bool any = false;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) any |= flags[w] != 0;
+    __syncthreads();
+    if (any) {
+#pragma unroll
+      for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+        for (int qh = 0; qh < kQH; ++qh) o[dt][qh] = f32x4{};
+#pragma unroll
+      for (int qh = 0; qh < kQH; ++qh) l_run[qh] = 0.0f;
+      key_loop(std::true_type{});
     }
   }
 
