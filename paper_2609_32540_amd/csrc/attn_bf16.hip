@@ -93,8 +93,10 @@ constexpr int kBlockQ = kWaves * kWaveQ;    // queries per workgroup
 constexpr int kBK = 64;                     // keys per tile
 constexpr int kXcds = 8;
 constexpr float kSumLimit = 16.0f;          // checked pass: largest block sum of probabilities kept
-constexpr float kFastLimit = 256.0f;        // fast pass: largest block sum before the checked pass
+constexpr float kFastLimit = 0x1p64f;       // fast pass: largest row sum before the checked pass
+constexpr int kVReadsFirst = 0;            // V reads issued ahead of the first S^T product
 constexpr int kHalfVALU = 20;               // plain VALU of a query half: 8 fma + 8 add + 4 packs
+constexpr int kHalfVALUFast = 14;           // the same without the adds (fast pass)
 // Waves w and w + 4 share a SIMD and the issue arbiter favours the older one
 // (w < 4), which reaches each tile's barrier well ahead of its partner; the
 // tile copies are therefore all issued by waves 0-3, off the partner's path.
@@ -116,13 +118,29 @@ struct Cfg {
   static_assert(BLOCKS % kCopyWaves == 0, "every copying wave copies the same number of 1 KB blocks");
 };
 
-// 16 bytes per lane from global memory (uniform base + per-lane byte offset)
-// straight into LDS at dst + 16 * lane.  Written out so that the compiler does
-// not track these copies: their completion is waited for explicitly (vmcnt)
-// before the barrier that hands a tile to the other waves.
-__device__ inline void lds_copy16(uint32_t dst, const char* base, uint32_t off) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
-               :: "s"(dst), "v"(off), "s"(base) : "memory");
+// N 1 KB copies from global memory straight into LDS: copy i takes 16 bytes
+// per lane from base + off[i] + 1024 i into LDS at dst + 1024 i + 16 lane.  The
+// instruction's immediate offset moves both addresses, so m0 (the LDS base) is
+// written once for all N; callers fold -1024 i into off[i] and lower base by
+// 1024 (N - 1) so that every per-lane offset stays non-negative.  Written out so
+// that the compiler does not track these copies: their completion is waited
+// for explicitly (vmcnt) before the barrier that hands a tile to the other
+// waves.
+template <int N>
+__device__ inline void lds_copy_blocks(uint32_t dst, const char* base, const uint32_t (&off)[N]) {
+  static_assert(N == 2 || N == 4, "two or four 1 KB copies per wave and tensor");
+  if constexpr (N == 2)
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\t"
+                 "global_load_lds_dwordx4 %1, %3\n\t"
+                 "global_load_lds_dwordx4 %2, %3 offset:1024"
+                 :: "s"(dst), "v"(off[0]), "v"(off[1]), "s"(base) : "memory");
+  else
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\t"
+                 "global_load_lds_dwordx4 %1, %5\n\t"
+                 "global_load_lds_dwordx4 %2, %5 offset:1024\n\t"
+                 "global_load_lds_dwordx4 %3, %5 offset:2048\n\t"
+                 "global_load_lds_dwordx4 %4, %5 offset:3072"
+                 :: "s"(dst), "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "s"(base) : "memory");
 }
 
 __device__ inline uint32_t pack_bf16(float a, float b) {
@@ -160,32 +178,34 @@ constexpr int waitcnt_vm(int vm) { return (vm & 15) | ((vm >> 4) << 14) | (7 << 
 
 // Instruction order of one half of a pipeline step, by sched_group_barrier
 // classes (0x008 matrix, 0x100 LDS read, 0x002 VALU, 0x400 transcendental):
-// NM products, each followed by its share of the half's NR LDS reads and of
-// the softmax of one query half (NV plain VALU instructions: 8 fma, 8 add, 4
-// packs and some slack; 8 exponentials), a few softmax instructions ahead of
-// the first product.
-template <int NM, int NR, int NV, int NT, int I>
+// NRF of the half's NR LDS reads and a few softmax instructions ahead of the
+// first product, then NM products, the first NR - NRF of them each followed by
+// one more LDS read, and all of them by their share of the softmax of one query
+// half (NV plain VALU instructions: 8 fma, 8 add, 4 packs and some slack; 8
+// exponentials).
+template <int NM, int NR, int NRF, int NV, int NT, int I>
 __device__ __forceinline__ void interleave_one() {
   __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-  constexpr int r = (NR * (I + 1)) / NM - (NR * I) / NM;
-  if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);
+  if constexpr (I < NR - NRF) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   constexpr int v = (NV * (I + 1)) / NM - (NV * I) / NM;
   if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x002, v, 0);
   constexpr int t = (NT * (I + 1)) / NM - (NT * I) / NM;
   if constexpr (t > 0) __builtin_amdgcn_sched_group_barrier(0x400, t, 0);
 }
 
-template <int NM, int NR, int NV, int NT, int... I>
+template <int NM, int NR, int NRF, int NV, int NT, int... I>
 __device__ __forceinline__ void interleave_seq(std::integer_sequence<int, I...>) {
-  (interleave_one<NM, NR, NV, NT, I>(), ...);
+  (interleave_one<NM, NR, NRF, NV, NT, I>(), ...);
 }
 
-template <int NM, int NR, int NV>
+template <int NM, int NR, int NRF, int NV>
 __device__ __forceinline__ void interleave_half() {
+  static_assert(NR - NRF <= NM, "every spread LDS read follows its own product");
   constexpr int kHead = 2, kHeadT = 1;
+  if constexpr (NRF > 0) __builtin_amdgcn_sched_group_barrier(0x100, NRF, 0);
   __builtin_amdgcn_sched_group_barrier(0x002, kHead, 0);
   __builtin_amdgcn_sched_group_barrier(0x400, kHeadT, 0);
-  interleave_seq<NM, NR, NV - kHead, 8 - kHeadT>(std::make_integer_sequence<int, NM>{});
+  interleave_seq<NM, NR, NRF, NV - kHead, 8 - kHeadT>(std::make_integer_sequence<int, NM>{});
 }
 
 // Tile cursor over the key segments: tile = (segment, first key).
@@ -278,10 +298,12 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
 #pragma unroll
     for (int qh = 0; qh < kQH; ++qh) o[dt][qh] = f32x4{};
   float m_run[kQH], l_run[kQH];
+  f32x4 lsum[kQH];          // fast pass: row sums (every row of the tile holds the sum)
 #pragma unroll
   for (int qh = 0; qh < kQH; ++qh) {
     m_run[qh] = 0.0f;       // reference max of the scaled logits (log2 units)
-    l_run[qh] = 0.0f;       // this lane's partial sum of probabilities
+    l_run[qh] = 0.0f;       // checked pass: this lane's partial sum of probabilities
+    lsum[qh] = f32x4{};
   }
 
   // Segment table in registers: lane i holds segment i's length, tokens-stride
@@ -334,38 +356,36 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   //     2 dt and 2 dt + 1 at 16 (2 i) and 16 (2 i + 1); block b = (G, H) holds
   //     the lines of d tiles 4 H .. 4 H + 3, so lane l carries row 8 G + (l % 16) / 2,
   //     chunk 8 H + 2 (l / 16) + l % 2.
-  // A segment's rows are at most 2^31 bytes apart (the host limits a chunk to
-  // 2^31 elements), so each lane's source is a 32-bit byte offset from the
-  // segment's (uniform) head base; rows past a partial tile's end re-read its
-  // last row, whose scores are masked.  The per-lane offsets are recomputed per
-  // tile rather than held in registers across the loop.
+  // The tile's first row is folded into the (uniform) 64-bit source base, so
+  // each lane's source is a small 32-bit offset: its row within the tile times
+  // the segment's row stride, plus its chunk; rows past a partial tile's end
+  // re-read the segment's last row, whose scores are masked.
   auto issue_tile = [&](char* base, Cursor c) __attribute__((always_inline)) {
     if (wave >= kCopyWaves) return;
+    constexpr int N = C::BLOCKS_PER_WAVE;
+    constexpr uint32_t kSpan = 1024u * (N - 1);   // largest immediate offset
     int ln = lane;
     asm volatile("" : "+v"(ln));
-    const int len = seg_len(c.sg);
     const uint32_t row_bytes = uint32_t(__builtin_amdgcn_readlane(int(sg_row_bytes), c.sg));
-    const char* kb = reinterpret_cast<const char*>(readlane_u64(sg_k, c.sg));
-    const char* vb = reinterpret_cast<const char*>(readlane_u64(sg_v, c.sg));
-    const bool partial = c.k0 + kBK > len;
+    // rows past the segment's end (a partial tile) re-read its last row
+    const int last = seg_len(c.sg) - 1 - c.k0;
+    const uint64_t tile_off = uint64_t(c.k0) * row_bytes - kSpan;
+    const char* kb = reinterpret_cast<const char*>(readlane_u64(sg_k, c.sg) + tile_off);
+    const char* vb = reinterpret_cast<const char*>(readlane_u64(sg_v, c.sg) + tile_off);
+    uint32_t koff[N], voff[N];
 #pragma unroll
-    for (int i = 0; i < C::BLOCKS_PER_WAVE; ++i) {
-      const int blk = wave * C::BLOCKS_PER_WAVE + i;
+    for (int i = 0; i < N; ++i) {
+      const int blk = wave * N + i;
       const int kr = 16 * (blk / C::KGB) + (ln & 15);
       const int kch = 4 * (blk % C::KGB) + (ln >> 4);
       const int vr = 8 * (blk / C::VGB) + ((ln & 15) >> 1);
       const int vch = 8 * (blk % C::VGB) + 2 * (ln >> 4) + (ln & 1);
-      int ktok = c.k0 + kr, vtok = c.k0 + vr;
-      if (partial) {
-        ktok = min(ktok, len - 1);
-        vtok = min(vtok, len - 1);
-      }
-      const uint32_t koff = uint32_t(ktok) * row_bytes + 16u * uint32_t(kch);
-      const uint32_t voff = uint32_t(vtok) * row_bytes + 16u * uint32_t(vch);
-      const uint32_t dst = uint32_t(size_t(LDS_PTR(char, base))) + blk * 1024;
-      lds_copy16(dst, kb, koff);
-      lds_copy16(dst + C::TILE, vb, voff);
+      koff[i] = uint32_t(min(kr, last)) * row_bytes + (16u * kch + kSpan - 1024u * i);
+      voff[i] = uint32_t(min(vr, last)) * row_bytes + (16u * vch + kSpan - 1024u * i);
     }
+    const uint32_t dst = uint32_t(size_t(LDS_PTR(char, base))) + wave * N * 1024;
+    lds_copy_blocks<N>(dst, kb, koff);
+    lds_copy_blocks<N>(dst + C::TILE, vb, voff);
   };
 
   // LDS read addresses.  The swizzle only flips chunk bits that the row offset
@@ -420,8 +440,11 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       a[dt] = __builtin_bit_cast(bf16x8, au);
     }
   };
-  // O^T += V^T P^T for one block
-  auto pv_mma = [&](const bf16x8 (&a)[C::DT], const uint32_t (&pk)[kQH][4]) __attribute__((always_inline)) {
+  // O^T += V^T P^T for one block; with_sums also adds the block's row sums into
+  // lsum (an all-ones A operand: every row of the 16 x 16 result is the column
+  // sum of P^T, i.e. the sum of exactly the rounded probabilities O^T adds up)
+  auto pv_mma = [&](const bf16x8 (&a)[C::DT], const uint32_t (&pk)[kQH][4], auto with_sums)
+      __attribute__((always_inline)) {
     bf16x8 pb[kQH];
 #pragma unroll
     for (int qh = 0; qh < kQH; ++qh) {
@@ -433,6 +456,13 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
 #pragma unroll
       for (int qh = 0; qh < kQH; ++qh)
         o[dt][qh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[dt], pb[qh], o[dt][qh], 0, 0, 0);
+    if constexpr (decltype(with_sums)::value) {
+      const bf16x8 ones = {__bf16(1.0f), __bf16(1.0f), __bf16(1.0f), __bf16(1.0f),
+                           __bf16(1.0f), __bf16(1.0f), __bf16(1.0f), __bf16(1.0f)};
+#pragma unroll
+      for (int qh = 0; qh < kQH; ++qh)
+        lsum[qh] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[qh], lsum[qh], 0, 0, 0);
+    }
   };
   // mask keys >= n_valid of a 32-key block
   auto mask_blk = [&](f32x4 (&s)[2][kQH], int n_valid) __attribute__((always_inline)) {
@@ -451,10 +481,10 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
     return max_across_groups(mx);
   };
   // probabilities of query half qh of a block as packed bf16: pk[qh] is the
-  // P^T operand of that half, keys 4 grp .. 4 grp+3 then 16 + 4 grp .. +3; lb[qh]
-  // is this lane's share of the block's row sum
-  auto p_half = [&](const f32x4 (&s)[2][kQH], int qh, uint32_t (&pk)[kQH][4], float (&lb)[kQH])
-      __attribute__((always_inline)) {
+  // P^T operand of that half, keys 4 grp .. 4 grp+3 then 16 + 4 grp .. +3; with
+  // with_sums, lb[qh] is this lane's share of the block's row sum
+  auto p_half = [&](const f32x4 (&s)[2][kQH], int qh, uint32_t (&pk)[kQH][4], float (&lb)[kQH],
+                    auto with_sums) __attribute__((always_inline)) {
     float sum = 0.0f;
 #pragma unroll
     for (int kh = 0; kh < 2; ++kh)
@@ -462,16 +492,15 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       for (int j = 0; j < 4; j += 2) {
         const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kh][qh][j], scale_log2, -m_run[qh]));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kh][qh][j + 1], scale_log2, -m_run[qh]));
-        const uint32_t w = pack_bf16(p0, p1);
-        pk[qh][2 * kh + (j >> 1)] = w;
-        sum += p0 + p1;
+        pk[qh][2 * kh + (j >> 1)] = pack_bf16(p0, p1);
+        if constexpr (decltype(with_sums)::value) sum += p0 + p1;
       }
-    lb[qh] = sum;
+    if constexpr (decltype(with_sums)::value) lb[qh] = sum;
   };
   auto p_blk = [&](const f32x4 (&s)[2][kQH], uint32_t (&pk)[kQH][4], float (&lb)[kQH])
       __attribute__((always_inline)) {
 #pragma unroll
-    for (int qh = 0; qh < kQH; ++qh) p_half(s, qh, pk, lb);
+    for (int qh = 0; qh < kQH; ++qh) p_half(s, qh, pk, lb, std::true_type{});
   };
   // The reference max is only raised when a block's probabilities (relative to
   // it) sum past kSumLimit: then the reference is raised to the block's column
@@ -514,53 +543,46 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   // the S^T products have just consumed), O^T += P(b-1) V(b-1) and the softmax
   // of query half 1.  Inside a half every product is followed by its share of
   // the LDS reads and of the softmax work (exponentials, row sums, bf16
-  // packing), which depends on no product of the step.
+  // packing), which depends on no product of the step.  The fast pass (with
+  // the checked tag false) sums the probabilities on the matrix core, the
+  // checked pass with VALU adds (its per-block check needs each block's sum).
   auto step = [&](bf16x8 (&ka)[2][C::KS], const char* vt, int kbv, const char* kt_next, int kb_next,
                   const f32x4 (&s_in)[2][kQH], f32x4 (&s_out)[2][kQH],
-                  const uint32_t (&pk_in)[kQH][4], uint32_t (&pk_out)[kQH][4], float (&lb)[kQH])
-      __attribute__((always_inline)) {
+                  const uint32_t (&pk_in)[kQH][4], uint32_t (&pk_out)[kQH][4], float (&lb)[kQH],
+                  auto checked) __attribute__((always_inline)) {
+    constexpr bool kChecked = decltype(checked)::value;
+    constexpr int kNV = kChecked ? kHalfVALU : kHalfVALUFast;
     bf16x8 va[C::DT];
     v_read(vt, kbv, va);
     s_mma(ka, s_out);
-    p_half(s_in, 0, pk_out, lb);
-    interleave_half<4 * C::KS, 2 * C::DT, kHalfVALU>();
+    p_half(s_in, 0, pk_out, lb, checked);
+    interleave_half<4 * C::KS, 2 * C::DT, kVReadsFirst, kNV>();
     __builtin_amdgcn_sched_barrier(0);
     k_read(kt_next, kb_next, ka);
-    pv_mma(va, pk_in);
-    p_half(s_in, 1, pk_out, lb);
-    interleave_half<2 * C::DT, 2 * C::KS, kHalfVALU>();
+    pv_mma(va, pk_in, std::bool_constant<!kChecked>{});
+    p_half(s_in, 1, pk_out, lb, checked);
+    interleave_half<2 * C::DT + (kChecked ? 0 : kQH), 2 * C::KS, 0, kNV>();
     // (the softmax results are computed inside this step, not sunk past the
     // branches that follow it)
     asm volatile("" ::"v"(pk_out[0][0]), "v"(pk_out[0][1]), "v"(pk_out[0][2]), "v"(pk_out[0][3]),
-                 "v"(pk_out[1][0]), "v"(pk_out[1][1]), "v"(pk_out[1][2]), "v"(pk_out[1][3]),
-                 "v"(lb[0]), "v"(lb[1]));
+                 "v"(pk_out[1][0]), "v"(pk_out[1][1]), "v"(pk_out[1][2]), "v"(pk_out[1][3]));
+    if constexpr (kChecked) asm volatile("" ::"v"(lb[0]), "v"(lb[1]));
     __builtin_amdgcn_sched_barrier(0);
   };
 
   // The key loop runs first as a fast pass: the reference max stays the first
-  // block's column max and a block only records whether its probabilities
-  // summed past kFastLimit (no branch).  Below that limit every probability is
-  // at most kFastLimit, nothing overflows, and how far the reference sits below
-  // the true max changes only the scale of O and l, not their ratio.  If any
-  // wave of the workgroup recorded an overflow (scores far above the first
-  // block's, or not finite), the workgroup runs its unit again as a checked
-  // pass, whose reference is raised per block (check_blk); strongly peaked rows
-  // thereby also get the reference at their largest score, where the dominant
-  // probability is exactly 1.
-  bool overflow = false;
+  // block's column max, the row sums come from the matrix core, and nothing is
+  // checked per block.  Since O and l then add exactly the same rounded
+  // probabilities, how far the reference sits below the true max changes only
+  // their common scale, as long as nothing overflows: a sum above kFastLimit
+  // (or one that is not finite) at the end of the pass sends the workgroup's
+  // unit through the key loop again as a checked pass, whose reference is
+  // raised per block (check_blk).
   auto key_loop = [&](auto checked) __attribute__((always_inline)) {
     constexpr bool kChecked = decltype(checked)::value;
     auto after_step = [&](const f32x4 (&s)[2][kQH], uint32_t (&pk)[kQH][4], float (&lb)[kQH])
         __attribute__((always_inline)) {
-      if constexpr (kChecked) {
-        check_blk(s, pk, lb);
-      } else {
-#pragma unroll
-        for (int qh = 0; qh < kQH; ++qh) {
-          overflow |= !(lb[qh] <= kFastLimit);   // (a NaN sum counts as an overflow)
-          l_run[qh] += lb[qh];
-        }
-      }
+      if constexpr (kChecked) check_blk(s, pk, lb);
     };
 
     // ---- prologue: tiles 0 .. 2 in flight, S^T of block 0 ----------------------
@@ -627,7 +649,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       }
       char* st = slot(i0);
       char* sn = slot(i1);
-      step(ka, (t == 0 ? st : slot(i4)) + C::TILE, 1, sn, 0, s_a, s_b, pk_b, pk_a, lb);
+      step(ka, (t == 0 ? st : slot(i4)) + C::TILE, 1, sn, 0, s_a, s_b, pk_b, pk_a, lb, checked);
       if (nv < kBK) mask_blk(s_b, nv - 32);   // keys past a segment's end
       after_step(s_a, pk_a, lb);
       int nv_next = 32;   // valid keys of tile t+1 (no mask after the last tile)
@@ -635,7 +657,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
         c_t = advance(c_t);
         nv_next = min(kBK, seg_len(c_t.sg) - c_t.k0);
       }
-      step(ka, st + C::TILE, 0, sn, 1, s_b, s_a, pk_a, pk_b, lb);
+      step(ka, st + C::TILE, 0, sn, 1, s_b, s_a, pk_a, pk_b, lb, checked);
       if (nv_next < 32) mask_blk(s_a, nv_next);
       after_step(s_b, pk_b, lb);
       nv = nv_next;
@@ -645,15 +667,28 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       // O^T += P(2n-1) V(2n-1): block 1 of the last tile
       bf16x8 va[C::DT];
       v_read(slot(i0 == 0 ? 4 : i0 - 1) + C::TILE, 1, va);
-      pv_mma(va, pk_b);
+      pv_mma(va, pk_b, std::bool_constant<!kChecked>{});
     }
   };
 
-  key_loop(std::false_type{});
-  // One flag per wave through LDS (the tiles are no longer read after the
-  // first barrier; the last one keeps the flags from being overwritten by the
-  // checked pass's copies before every wave has read them).
-  {
+  // A launch that also writes the log-sum-exp (the packed forward of the
+  // training path) runs the checked pass only: its row sums are float32 sums of
+  // the unrounded probabilities, as the backward's log-sum-exp is defined.
+  bool exact_sums = false;
+  if constexpr (kPacked) exact_sums = src.lse != nullptr;
+  float l_tot[kQH];   // the row sum of the lane's query
+  bool checked_pass = true;
+  if (!exact_sums) {
+    key_loop(std::false_type{});
+    bool overflow = false;
+#pragma unroll
+    for (int qh = 0; qh < kQH; ++qh) {
+      l_tot[qh] = lsum[qh][0];
+      overflow |= !(l_tot[qh] <= kFastLimit);   // (a NaN sum counts as an overflow)
+    }
+    // One flag per wave through LDS (the tiles are no longer read after the
+    // first barrier; the last one keeps the flags from being overwritten by
+    // the checked pass's copies before every wave has read them).
     const bool mine = __builtin_amdgcn_ballot_w64(overflow) != 0;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
@@ -664,15 +699,18 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) any |= flags[w] != 0;
     __syncthreads();
+    checked_pass = any;
     if (any) {
 #pragma unroll
       for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
         for (int qh = 0; qh < kQH; ++qh) o[dt][qh] = f32x4{};
-#pragma unroll
-      for (int qh = 0; qh < kQH; ++qh) l_run[qh] = 0.0f;
-      key_loop(std::true_type{});
     }
+  }
+  if (checked_pass) {
+    key_loop(std::true_type{});
+#pragma unroll
+    for (int qh = 0; qh < kQH; ++qh) l_tot[qh] = sum_across_groups(l_run[qh]);
   }
 
   // normalise and store: lane (l16, grp) of tile (dt, qh) holds query
@@ -680,12 +718,11 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
 #pragma unroll
   for (int qh = 0; qh < kQH; ++qh) {
     const int qi = q0 + 16 * qh + l16;
-    const float l_tot = sum_across_groups(l_run[qh]);
-    const float inv = 1.0f / l_tot;
+    const float inv = 1.0f / l_tot[qh];
     if constexpr (kPacked) {
       // base-2 log-sum-exp of the scaled logits, for the backward pass
       if (src.lse != nullptr && grp == 0 && qi < nq)
-        src.lse[(int64_t(chunk) * nq + qi) * heads + head] = m_run[qh] + log2f(l_tot);
+        src.lse[(int64_t(chunk) * nq + qi) * heads + head] = m_run[qh] + log2f(l_tot[qh]);
     }
     if (n_parts > 1) {
       // unnormalised partial result of this part: O (row = query of the
@@ -698,7 +735,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
         *reinterpret_cast<f32x4*>(pb + row * D + 16 * dt + 4 * grp) = o[dt][qh];
       if (grp == 0) {
         pb[kBlockQ * D + row] = m_run[qh];
-        pb[kBlockQ * D + kBlockQ + row] = l_tot;
+        pb[kBlockQ * D + kBlockQ + row] = l_tot[qh];
       }
     } else if (qi < nq) {
       __bf16* op = out + (int64_t(qi) * heads + head) * D + 4 * grp;
