@@ -96,7 +96,7 @@ constexpr float kSumLimit = 16.0f;          // checked pass: largest block sum o
 constexpr float kFastLimit = 0x1p64f;       // fast pass: largest row sum before the checked pass
 constexpr int kVReadsFirst = 0;            // V reads issued ahead of the first S^T product
 constexpr int kHalfVALU = 20;               // plain VALU of a query half: 8 fma + 8 add + 4 packs
-constexpr int kHalfVALUFast = 14;           // the same without the adds (fast pass)
+constexpr int kHalfVALUFast = 16;           // the fast pass: 8 fma + 4 packs and slack
 // Waves w and w + 4 share a SIMD and the issue arbiter favours the older one
 // (w < 4), which reaches each tile's barrier well ahead of its partner; the
 // tile copies are therefore all issued by waves 0-3, off the partner's path.
