@@ -279,6 +279,32 @@ def test_attention_running_max_rescales(head_dim, heads, grid):
         hist = (hist + [(exact(k), exact(v))])[-W:]
 
 
+@pytest.mark.parametrize("head_dim", [128, 64])
+def test_attention_reference_far_below_the_max(head_dim):
+    # The first chunk's keys are tiny, so the first block a later chunk reads
+    # (its oldest history chunk, or itself for chunk 0) gives a reference max
+    # near 0 while the largest scores sit far above it: keys scaled by 8 give
+    # probabilities up to ~2^35 relative to that reference (strongly peaked
+    # rows, no overflow), keys scaled by 24 go past 2^64 (the workgroup's unit
+    # runs again with the reference raised per block).
+    W = 4
+    w = small("bf16", head_dim, heads=2, grid_h=6, grid_w=11, ring_chunks=W,
+              stages=1, layers=1, n_chunks=5, anchor_rule="none", max_anchor_frames=1)
+    cache = make_cache(w, 1, 1)
+    hist = []
+    for c, factor in enumerate([0.01, 8.0, 8.0, 24.0, 1.0]):
+        q, k, v = (synth.chunk_tensor(w, t, c, 0, 0) for t in (synth.T_Q, synth.T_K, synth.T_V))
+        k = (k.float() * factor).to(torch.bfloat16)
+        out = cache.chunk_attention(0, 0, c, to_dev(q), to_dev(k), to_dev(v))
+        cache.kv_publish(0, 0, c, to_dev(k), to_dev(v))
+        K_all = np.concatenate([h[0] for h in hist] + [exact(k)])
+        V_all = np.concatenate([h[1] for h in hist] + [exact(v)])
+        ref = fo.masked_attention(exact(q), K_all, V_all, np.ones(len(K_all), bool),
+                                  1.0 / math.sqrt(head_dim))
+        check_attention(exact(out), ref, "bf16", f"chunk {c} (key scale {factor:g})")
+        hist = (hist + [(exact(k), exact(v))])[-W:]
+
+
 @pytest.mark.parametrize("dtype,head_dim", [("bf16", 128), ("bf16", 64), ("f32", 64)])
 def test_attention_batch_equals_single_calls(dtype, head_dim):
     # the rounds of a 4-stage wavefront (round n: chunk n - s at stage s), each
