@@ -8,45 +8,44 @@
 // segments and no empty slot is touched.
 //
 // Products, per 32-key block (two per tile), all on v_mfma_f32_16x16x32_bf16
-// (16 x 16 outputs, 32-deep sums):
+// (16 x 16 outputs, 32-deep sums: the least register traffic per FLOP of the
+// bf16 shapes, which matters because the kernel runs power-limited):
 //   S^T = K Q^T     four 16 x 16 tiles (key half kh x query half qh), four
 //                   32-wide d slices each; A = K rows read from LDS, B = the
 //                   wave's Q^T, held in registers for the whole loop.
 //   softmax         lane (n, g) = (lane % 16, lane / 16) holds, for query n of
-//                   each query half, keys 4g .. 4g+3 of each key half, so a
-//                   query's row sum stays in-lane until a final reduction over
-//                   the four lane groups.  p = exp2(s c - m) with c = scale *
-//                   log2 e applied in float32 (one fma; Q is not rounded again
-//                   after scaling).  The reference max m is the
-//                   first block's column max and is only raised when a block's
-//                   probabilities sum past kSumLimit (every kept probability is
-//                   then at most kSumLimit, and infinities from scores far above
-//                   the reference trip the same test): that rare block is
-//                   recomputed from LDS, O and l rescaled and its probabilities
-//                   redone.  The result is exact for any reference, since the
-//                   final sum uses the same one; no column max is taken per block.
+//                   each query half, keys 4g .. 4g+3 of each key half.
+//                   p = exp2(s c - m) with c = scale * log2 e applied in
+//                   float32 (one fma; Q is not rounded again after scaling).
 //   O^T += V^T P^T  16-row d tiles x query halves, one 32-deep sum per block;
 //                   A = V^T, read from the row-major V tile with the gfx950
 //                   transposing LDS read (ds_read_b64_tr_b16); B = P^T, the
-//                   softmax registers rounded to bf16 in place.  The sum runs
-//                   over the keys in the order the softmax registers hold them
-//                   (lane group g: keys 4g .. 4g+3, then 16+4g .. 16+4g+3).
-// Software pipeline over blocks b: A(b) computes S^T of block b+1 on the matrix
-// core beside the exponentials of block b; B(b) checks block b's sum, adds
-// block b into O^T and masks block b+1 if it is partial.  Waves w and w + 4
-// share a SIMD: waves 0-3 run A(2t) B(2t) A(2t+1) B(2t+1) after barrier t,
-// waves 4-7 run one phase later, B(2t-1) A(2t) B(2t) A(2t+1), so on every SIMD
-// one wave's exponentials run beside the other's matrix work.
+//                   softmax registers rounded to bf16.  The sum runs over the
+//                   keys in the order the softmax registers hold them (lane
+//                   group g: keys 4g .. 4g+3, then 16+4g .. 16+4g+3).
+// Each 32-key step of a wave issues S^T of block b+1 and O^T += P(b-1) V(b-1)
+// and places the softmax of block b, which depends on neither, product by
+// product between them: a wave's own VALU work overlaps its matrix work far
+// better than one wave's VALU work overlaps its SIMD partner's products.  A
+// step is two scheduling halves (V reads, S^T products, softmax of query half
+// 0 | K reads of the next step, P V products, softmax of query half 1), so the
+// next step's K reads cannot be hoisted above the products that still use
+// their registers.
+// The key loop first runs as a fast pass: the reference max m stays the first
+// block's column max and the row sums come from the matrix core (an all-ones A
+// operand sums exactly the rounded probabilities the P V products add), so O
+// and l share one scale however far m sits below the true max.  A row sum
+// above kFastLimit (or not finite) sends the workgroup's unit through the loop
+// again as a checked pass that raises m per block (check_blk); launches that
+// write the log-sum-exp use the checked pass only.
 // K and V tiles are copied from HBM straight into LDS (global_load_lds_dwordx4,
-// 16 bytes per lane) by waves 0-3 at the end of their step t, three tiles
-// ahead, into a ring of five tile slots (all 160 KB of LDS at d = 128): the
-// slot of tile t+3 held tile t-2, whose last read (waves 4-7, B(2t-3)) came
-// before barrier t.  Barrier t waits only for the copy of tile t+1, so each
-// copy has a whole step to land.  The copies are issued from inline assembly
-// and waited for explicitly, so the compiler does not add its own conservative
-// waits for them.  Every LDS read is a per-lane base plus immediates except
-// for the slot base, added once per phase, so the tile loop stays rolled
-// (the kernel's hot code is a few KB).
+// 16 bytes per lane) by waves 0-3, three tiles ahead, into a ring of five tile
+// slots (all 160 KB of LDS at d = 128): after barrier t (tile t+1 has landed,
+// tile t-2 is no longer read) tile t+3 goes into tile t-2's slot.  The copies
+// are issued from inline assembly and waited for explicitly, so the compiler
+// does not add its own conservative waits for them.  Every LDS read is a
+// per-lane base plus immediates except for the slot base, so the tile loop
+// stays rolled.
 // The tiles are stored without padding in layouts chosen for their reads: a K
 // tile chunk-major per 16 keys (one 256-byte line per 16-byte chunk of 16
 // keys), a V tile d-blocked (one 256-byte line per 8 keys and 16-wide d tile).
