@@ -431,7 +431,11 @@ def measure_steps(w: synth.Workload, steps: int, warmup: int) -> dict:
         cold[l][1].record(stream)
     torch.cuda.synchronize()
     pub_cold = float(np.mean([e[0].elapsed_time(e[1]) for e in cold]))
+    # per-step durations (first event of the step's first layer to the last
+    # event of its last layer) for the spread over the timed steps
+    step_ms = [events[k][0][0].elapsed_time(events[k][-1][3]) for k in range(steps)]
     res = dict(ms_total=ms_total, flops=flops, chunks=chunks,
+               step_ms_std=float(np.std(step_ms)), attn_ms_std=float(np.std(attn_ms)),
                attn_ms=float(np.mean(attn_ms)), pub_ms=float(np.mean(pub_ms)),
                rope_ms=float(np.mean(rope_ms)), pub_cold_ms=pub_cold,
                attn_flops=float(np.mean(attn_flops)),
@@ -461,12 +465,14 @@ def summarize(w: synth.Workload, m: dict, steps: int) -> dict:
         "kv_tokens": m["kv_tokens"], "ring_chunks": w.ring_chunks, "stages": w.stages,
         "layers": w.layers, "anchor_frames": m["anchor_frames"], "steps": steps,
         "ms_per_step": round(m["ms_total"] / steps, 3),
+        "ms_per_step_std": round(m["step_ms_std"], 3),
         "tflops_step": round(value, 2),
         "ms_attn_per_chunk_stage": round(m["attn_ms"] * w.layers, 3),
         "ms_attn_target_at_50pct_peak": round(target, 3),
         "ms_attn_publish_per_chunk_stage": round((m["attn_ms"] + m["pub_ms"]) * w.layers, 3),
         "ms_rope_per_chunk_stage": round(m["rope_ms"] * w.layers, 3),
-        "attention": {"ms_per_launch": round(m["attn_ms"], 4), "tflops": round(tf, 2),
+        "attention": {"ms_per_launch": round(m["attn_ms"], 4), "ms_per_launch_std": round(m["attn_ms_std"], 4),
+                      "tflops": round(tf, 2),
                       "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2)},
         "kv_publish": {"us_per_launch": round(m["pub_ms"] * 1e3, 2), "gbs": round(gbs["pub_ms"], 1),
                        "pct_hbm_peak": round(100 * gbs["pub_ms"] / PEAK_HBM_GBS, 2),
@@ -559,8 +565,8 @@ def host_cpu() -> dict:
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=8)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="14b-720p", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--configs", default="1.3b-480p,14b-480p",
                     help="other chunk-stage workloads to time beside the headline ('' for none)")
@@ -621,6 +627,7 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": head["ms_per_step"],
+        "ms_per_step_std": head["ms_per_step_std"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
