@@ -171,7 +171,7 @@ struct Stream {
 // work on tile t-1 while waves 0-3 work on tile t.  Slots are distinct __shared__ arrays, referenced
 // statically (the loops are unrolled by NS), so the compiler never orders a
 // read of one slot behind a copy into another.
-template <int NS, int kBlocks, class Issue, class NextNv, class Block>
+template <int NS, int kBlocks, int kPerTile, class Issue, class NextNv, class Block>
 __device__ __attribute__((always_inline)) inline void run_ring(int n, int wave, char* s0, char* s1,
                                                                char* s2, char* s3, Issue& issue,
                                                                NextNv& next_nv, Block& block) {
@@ -179,6 +179,26 @@ __device__ __attribute__((always_inline)) inline void run_ring(int n, int wave, 
   auto sync = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+  };
+  // Barrier of a copying wave before step t when tiles are copied two ahead:
+  // tile t must have landed, but tile t + 1 (issued after it, at least
+  // kPerTile memory instructions) may stay in flight if it was issued at all
+  // (t + 1 < n).  A bare s_barrier, since the workgroup fence of
+  // __syncthreads would wait for every copy.
+  static_assert(R::kAhead <= 2, "at most one tile in flight past the one read next");
+  constexpr int kKeep = (R::kAhead - 1) * kPerTile;
+  static_assert(kKeep < 16, "vmcnt field");
+  auto copy_sync = [&](int t) __attribute__((always_inline)) {
+    if constexpr (kKeep == 0) {
+      sync();
+    } else {
+      // vmcnt = kKeep or 0, lgkmcnt = 0, expcnt not waited for
+      if (t + 1 < n)
+        __builtin_amdgcn_s_waitcnt(kKeep | (7 << 4));
+      else
+        __builtin_amdgcn_s_waitcnt(7 << 4);
+      asm volatile("s_barrier" ::: "memory");
+    }
   };
   if constexpr (!R::kOffset) {
     issue(s0);
@@ -199,7 +219,7 @@ __device__ __attribute__((always_inline)) inline void run_ring(int n, int wave, 
     issue(s0);
     if (R::kAhead > 1 && n > 1) issue(s1);
     auto step = [&](int t, char* cur, char* ahead) __attribute__((always_inline)) {
-      sync();
+      copy_sync(t);
       if (t + R::kAhead < n) issue(ahead);
       const int nv = next_nv();
       block(cur, 0, nv);
@@ -288,22 +308,27 @@ __device__ __attribute__((always_inline)) inline void run_ring(int n, int wave, 
 
 // acc[kb] = A(rows kb*32 .. +31 of the tile) x B^T, B the stationary operand
 // (lane (l32, half) holds column l32, elements 16 ks + 8 half .. +7)
-template <int D>
+// (kInit: added to the accumulator's initial value; kPattern: with its own
+// read-ahead schedule)
+template <int D, bool kInit = false, bool kPattern = true>
 __device__ inline void rows_times_b(const char* tile, int kb, int a_lane, const bf16x8 (&breg)[D / 16],
                                     f32x16& acc) {
+  if constexpr (!kInit)
 #pragma unroll
-  for (int j = 0; j < 16; ++j) acc[j] = 0.0f;
+    for (int j = 0; j < 16; ++j) acc[j] = 0.0f;
   const char* base = tile + kb * 32 * Cfg<D>::ROWB;
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks) {
     const bf16x8 a = *reinterpret_cast<const bf16x8*>(base + (a_lane ^ (ks << 5)));
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, breg[ks], acc, 0, 0, 0);
   }
-  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  if constexpr (kPattern) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
-    if (ks + 2 < D / 16) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    for (int ks = 0; ks < D / 16; ++ks) {
+      if (ks + 2 < D / 16) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
   }
 }
 
@@ -377,7 +402,8 @@ __device__ inline void stash_b(char* stat, const __bf16* base, int64_t row_elems
 }
 
 // acc = A(rows kb*32 .. +31 of the tile) x B^T with B read from the stash
-template <int D>
+// (kPattern: with its own read-ahead schedule)
+template <int D, bool kPattern = true>
 __device__ inline void rows_times_stash(const char* tile, int kb, int a_lane, const char* stat_w,
                                         f32x16& acc) {
 #pragma unroll
@@ -389,12 +415,14 @@ __device__ inline void rows_times_stash(const char* tile, int kb, int a_lane, co
     const bf16x8 b = *reinterpret_cast<const bf16x8*>(stat_w + (a_lane ^ (ks << 5)));
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
   }
-  // operands read two products ahead at most (register budget)
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+  if constexpr (kPattern) {
+    // operands read two products ahead at most (register budget)
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
-    if (ks + 2 < D / 16) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    for (int ks = 0; ks < D / 16; ++ks) {
+      if (ks + 2 < D / 16) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
   }
 }
 
@@ -537,7 +565,8 @@ __device__ __attribute__((always_inline)) inline void dq_body(
     rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);                     // dQ^T += K^T dS^T
     __builtin_amdgcn_sched_barrier(0);   // one 32-key block at a time (register budget)
   };
-  if (st.n_tiles > 0) run_ring<NS, 2>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv, block);
+  if (st.n_tiles > 0)
+    run_ring<NS, 2, 2 * decltype(st)::BPW>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv, block);
   store_t<D>(dq + tok0 * row_elems + head * D, row_elems, q0 + l32, nq, lane, acc, scale);
 }
 
@@ -667,41 +696,84 @@ __device__ __attribute__((always_inline)) inline void dkv_body(
     st.advance(csg, ck0);
     return nv;
   };
+  // One 32-query block in four scheduling regions: (1) S - L / c (L / c as the
+  // accumulator's initial value); (2) dP, with P = 2^(c (S - L / c)) computed
+  // under its products; (3) dV^T += dO^T P, with dS = P (dP - D) computed and
+  // packed under its products; (4) dK^T += Q^T dS.
+  const float neg_inv_c = -1.0f / c_log2;
   auto block = [&](const char* cur, int kb, int nv) __attribute__((always_inline)) {
     // keep the per-read address arithmetic inside the loop (no hoisted copies)
     asm volatile("" : "+v"(ln.a_lane), "+v"(ln.t_lane[0]), "+v"(ln.t_lane[1]));
     const float* lse_t = reinterpret_cast<const float*>(cur + 2 * C::TILE);
     const float* del_t = reinterpret_cast<const float*>(cur + 2 * C::TILE + C::VEC);
+    const int row0 = kb * 32 + 4 * half;   // register 4 g + e: row row0 + 8 g + e
     f32x16 sv;
-    rows_times_b<D>(cur, kb, ln.a_lane, kreg, sv);                // S = Q K^T (rows = queries)
-    __builtin_amdgcn_sched_barrier(0);
-    f32x16 dp;
-    rows_times_stash<D>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);   // dP = dO V^T
-    __builtin_amdgcn_sched_barrier(0);
-    uint32_t pk[8], pv[8];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int r0 = kb * 32 + 8 * g + 4 * half;
-      const f32x4 Lr = *reinterpret_cast<const f32x4*>(lse_t + r0);
-      const f32x4 Dr = *reinterpret_cast<const f32x4*>(del_t + r0);
-      float v4[4], p4[4];
+      const f32x4 Lr = *reinterpret_cast<const f32x4*>(lse_t + row0 + 8 * g);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p = r0 + e < nv ? __builtin_amdgcn_exp2f(fmaf(sv[4 * g + e], c_log2, -Lr[e])) : 0.0f;
-        p4[e] = p;
-        v4[e] = p * (dp[4 * g + e] - Dr[e]);
-      }
-      pk[2 * g] = pack_bf16(v4[0], v4[1]);
-      pk[2 * g + 1] = pack_bf16(v4[2], v4[3]);
-      pv[2 * g] = pack_bf16(p4[0], p4[1]);
-      pv[2 * g + 1] = pack_bf16(p4[2], p4[3]);
+      for (int e = 0; e < 4; ++e) sv[4 * g + e] = Lr[e] * neg_inv_c;
     }
-    // dV^T += dO^T P, dK^T += Q^T dS
-    rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc_v);
-    rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);
+    rows_times_b<D, true, false>(cur, kb, ln.a_lane, kreg, sv);   // S - L / c (rows = queries)
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);   // L and the first two operands
+    __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (ks + 2 < C::KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    f32x16 dp;
+    rows_times_stash<D, false>(cur + C::TILE, kb, ln.a_lane, stash_w, dp);   // dP = dO V^T
+    float p[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) p[j] = __builtin_amdgcn_exp2f(sv[j] * c_log2);
+    // the first two products' operands; then per product two reads, two
+    // multiplies and two exponentials
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (ks + 2 < C::KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (nv < BT) {   // rows past a partial tile's end
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+        if (row0 + 8 * (j >> 2) + (j & 3) >= nv) p[j] = 0.0f;
+    }
+    uint32_t pk[8], pv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pv[i] = pack_bf16(p[2 * i], p[2 * i + 1]);
+    rows_t_times_p<D>(cur + C::TILE, kb, ln.t_lane, pv, acc_v);   // dV^T += dO^T P
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 Dr = *reinterpret_cast<const f32x4*>(del_t + row0 + 8 * g);
+      float ds[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ds[e] = p[4 * g + e] * (dp[4 * g + e] - Dr[e]);
+      pk[2 * g] = pack_bf16(ds[0], ds[1]);
+      pk[2 * g + 1] = pack_bf16(ds[2], ds[3]);
+    }
+    // D and the first two products' operands, the packs they need; then per
+    // product two reads and five VALU (the other packs, dS)
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+#pragma unroll
+    for (int i = 0; i < 2 * C::DB; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (i + 2 < 2 * C::DB) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    rows_t_times_p<D>(cur, kb, ln.t_lane, pk, acc);              // dK^T += Q^T dS
     __builtin_amdgcn_sched_barrier(0);   // one 32-query block at a time (register budget)
   };
-  if (st.n_tiles > 0) run_ring<NS, kBlocks>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv, block);
+  if (st.n_tiles > 0)
+    run_ring<NS, kBlocks, 2 * decltype(st)::BPW>(st.n_tiles, wave, s0, s1, s2, s3, issue, next_nv,
+                                                 block);
   store_t<D>(obase_k + head * D, row_elems, k0 + l32, n_keys, lane, acc, scale);
   store_t<D>(obase_v + head * D, row_elems, k0 + l32, n_keys, lane, acc_v, 1.0f);
 }
