@@ -211,8 +211,24 @@ def packed_clip(w: synth.Workload, reps: int = 3, backward: bool = True) -> dict
         # dK/dV pass, then dQ, dK, dV)
         lse = torch.empty((n * Nq, w.heads), dtype=torch.float32, device=dev)
         dout = torch.randn(shape, generator=g, device=dev).to(w.torch_dtype)
-        ff.packed_attention(q, k, v, n_chunks=n, window=w.ring_chunks, anchor_k=ak, anchor_v=av,
-                            frame_tokens=G, anchors_of_chunk=table, out=out, lse=lse)
+
+        def launch_lse():
+            ff.packed_attention(q, k, v, n_chunks=n, window=w.ring_chunks, anchor_k=ak, anchor_v=av,
+                                frame_tokens=G, anchors_of_chunk=table, out=out, lse=lse)
+        # the training forward: the same launch writing its log-sum-exp
+        launch_lse()
+        torch.cuda.synchronize()
+        evl = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        evl[0].record(stream)
+        for r in range(reps):
+            launch_lse()
+            evl[r + 1].record(stream)
+        torch.cuda.synchronize()
+        lms = float(np.mean([evl[r].elapsed_time(evl[r + 1]) for r in range(reps)]))
+        ltf = flops / (lms * 1e-3) / 1e12
+        log(f"packed clip attention with its log-sum-exp: {lms:.2f} ms = {ltf:.1f} TFLOP/s")
+        result["with_lse"] = {"ms_per_launch": round(lms, 3), "tflops": round(ltf, 2),
+                              "pct_bf16_peak": round(100 * ltf / PEAK_BF16_TFLOPS, 2)}
 
         def bwd():
             return ff.packed_attention_bwd(q, k, v, out, dout, lse, n_chunks=n, window=w.ring_chunks,

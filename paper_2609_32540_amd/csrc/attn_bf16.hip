@@ -36,8 +36,9 @@
 // operand sums exactly the rounded probabilities the P V products add), so O
 // and l share one scale however far m sits below the true max.  A row sum
 // above kFastLimit (or not finite) sends the workgroup's unit through the loop
-// again as a checked pass that raises m per block (check_blk); launches that
-// write the log-sum-exp use the checked pass only.
+// again as a checked pass that raises m per block (check_blk).  Launches that
+// write the log-sum-exp run the fast pass with float32 row sums of the
+// unrounded probabilities instead (the log-sum-exp's definition).
 // K and V tiles are copied from HBM straight into LDS (global_load_lds_dwordx4,
 // 16 bytes per lane) by waves 0-3, three tiles ahead, into a ring of five tile
 // slots (all 160 KB of LDS at d = 128): after barrier t (tile t+1 has landed,
@@ -93,6 +94,10 @@ constexpr int kBK = 64;                     // keys per tile
 constexpr int kXcds = 8;
 constexpr float kSumLimit = 16.0f;          // checked pass: largest block sum of probabilities kept
 constexpr float kFastLimit = 0x1p64f;       // fast pass: largest row sum before the checked pass
+// passes of the key loop
+constexpr int kPassFast = 0;       // fixed reference, row sums of the rounded P on the matrix core
+constexpr int kPassFastExact = 1;  // fixed reference, float32 row sums of the unrounded P
+constexpr int kPassChecked = 2;    // reference raised per block (check_blk)
 constexpr int kVReadsFirst = 0;            // V reads issued ahead of the first S^T product
 constexpr int kHalfVALU = 20;               // plain VALU of a query half: 8 fma + 8 add + 4 packs
 constexpr int kHalfVALUFast = 16;           // the fast pass: 8 fma + 4 packs and slack
@@ -542,30 +547,31 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   // the S^T products have just consumed), O^T += P(b-1) V(b-1) and the softmax
   // of query half 1.  Inside a half every product is followed by its share of
   // the LDS reads and of the softmax work (exponentials, row sums, bf16
-  // packing), which depends on no product of the step.  The fast pass (with
-  // the checked tag false) sums the probabilities on the matrix core, the
-  // checked pass with VALU adds (its per-block check needs each block's sum).
+  // packing), which depends on no product of the step.  The fast pass sums
+  // the probabilities on the matrix core, the other passes with VALU adds (the
+  // checked pass's per-block check needs each block's sum; the exact fast pass
+  // sums the unrounded probabilities).
   auto step = [&](bf16x8 (&ka)[2][C::KS], const char* vt, int kbv, const char* kt_next, int kb_next,
                   const f32x4 (&s_in)[2][kQH], f32x4 (&s_out)[2][kQH],
                   const uint32_t (&pk_in)[kQH][4], uint32_t (&pk_out)[kQH][4], float (&lb)[kQH],
-                  auto checked) __attribute__((always_inline)) {
-    constexpr bool kChecked = decltype(checked)::value;
-    constexpr int kNV = kChecked ? kHalfVALU : kHalfVALUFast;
+                  auto pass) __attribute__((always_inline)) {
+    constexpr bool kVSums = decltype(pass)::value != kPassFast;   // row sums in VALU
+    constexpr int kNV = kVSums ? kHalfVALU : kHalfVALUFast;
     bf16x8 va[C::DT];
     v_read(vt, kbv, va);
     s_mma(ka, s_out);
-    p_half(s_in, 0, pk_out, lb, checked);
+    p_half(s_in, 0, pk_out, lb, std::bool_constant<kVSums>{});
     interleave_half<4 * C::KS, 2 * C::DT, kVReadsFirst, kNV>();
     __builtin_amdgcn_sched_barrier(0);
     k_read(kt_next, kb_next, ka);
-    pv_mma(va, pk_in, std::bool_constant<!kChecked>{});
-    p_half(s_in, 1, pk_out, lb, checked);
-    interleave_half<2 * C::DT + (kChecked ? 0 : kQH), 2 * C::KS, 0, kNV>();
+    pv_mma(va, pk_in, std::bool_constant<!kVSums>{});
+    p_half(s_in, 1, pk_out, lb, std::bool_constant<kVSums>{});
+    interleave_half<2 * C::DT + (kVSums ? 0 : kQH), 2 * C::KS, 0, kNV>();
     // (the softmax results are computed inside this step, not sunk past the
     // branches that follow it)
     asm volatile("" ::"v"(pk_out[0][0]), "v"(pk_out[0][1]), "v"(pk_out[0][2]), "v"(pk_out[0][3]),
                  "v"(pk_out[1][0]), "v"(pk_out[1][1]), "v"(pk_out[1][2]), "v"(pk_out[1][3]));
-    if constexpr (kChecked) asm volatile("" ::"v"(lb[0]), "v"(lb[1]));
+    if constexpr (kVSums) asm volatile("" ::"v"(lb[0]), "v"(lb[1]));
     __builtin_amdgcn_sched_barrier(0);
   };
 
@@ -576,12 +582,18 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
   // their common scale, as long as nothing overflows: a sum above kFastLimit
   // (or one that is not finite) at the end of the pass sends the workgroup's
   // unit through the key loop again as a checked pass, whose reference is
-  // raised per block (check_blk).
-  auto key_loop = [&](auto checked) __attribute__((always_inline)) {
-    constexpr bool kChecked = decltype(checked)::value;
+  // raised per block (check_blk).  The exact fast pass differs only in its
+  // row sums: float32 sums of the unrounded probabilities (VALU adds).
+  auto key_loop = [&](auto pass) __attribute__((always_inline)) {
+    constexpr int kPass = decltype(pass)::value;
     auto after_step = [&](const f32x4 (&s)[2][kQH], uint32_t (&pk)[kQH][4], float (&lb)[kQH])
         __attribute__((always_inline)) {
-      if constexpr (kChecked) check_blk(s, pk, lb);
+      if constexpr (kPass == kPassChecked) {
+        check_blk(s, pk, lb);
+      } else if constexpr (kPass == kPassFastExact) {
+#pragma unroll
+        for (int qh = 0; qh < kQH; ++qh) l_run[qh] += lb[qh];
+      }
     };
 
     // ---- prologue: tiles 0 .. 2 in flight, S^T of block 0 ----------------------
@@ -648,7 +660,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       }
       char* st = slot(i0);
       char* sn = slot(i1);
-      step(ka, (t == 0 ? st : slot(i4)) + C::TILE, 1, sn, 0, s_a, s_b, pk_b, pk_a, lb, checked);
+      step(ka, (t == 0 ? st : slot(i4)) + C::TILE, 1, sn, 0, s_a, s_b, pk_b, pk_a, lb, pass);
       if (nv < kBK) mask_blk(s_b, nv - 32);   // keys past a segment's end
       after_step(s_a, pk_a, lb);
       int nv_next = 32;   // valid keys of tile t+1 (no mask after the last tile)
@@ -656,7 +668,7 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
         c_t = advance(c_t);
         nv_next = min(kBK, seg_len(c_t.sg) - c_t.k0);
       }
-      step(ka, st + C::TILE, 0, sn, 1, s_b, s_a, pk_a, pk_b, lb, checked);
+      step(ka, st + C::TILE, 0, sn, 1, s_b, s_a, pk_a, pk_b, lb, pass);
       if (nv_next < 32) mask_blk(s_a, nv_next);
       after_step(s_b, pk_b, lb);
       nv = nv_next;
@@ -666,25 +678,33 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       // O^T += P(2n-1) V(2n-1): block 1 of the last tile
       bf16x8 va[C::DT];
       v_read(slot(i0 == 0 ? 4 : i0 - 1) + C::TILE, 1, va);
-      pv_mma(va, pk_b, std::bool_constant<!kChecked>{});
+      pv_mma(va, pk_b, std::bool_constant<kPass == kPassFast>{});
     }
   };
 
   // A launch that also writes the log-sum-exp (the packed forward of the
-  // training path) runs the checked pass only: its row sums are float32 sums of
+  // training path) runs the exact fast pass: its row sums are float32 sums of
   // the unrounded probabilities, as the backward's log-sum-exp is defined.
   bool exact_sums = false;
   if constexpr (kPacked) exact_sums = src.lse != nullptr;
   float l_tot[kQH];   // the row sum of the lane's query
   bool checked_pass = true;
-  if (!exact_sums) {
-    key_loop(std::false_type{});
+  {
+    if (kPacked && exact_sums) {
+      if constexpr (kPacked) {
+        key_loop(std::integral_constant<int, kPassFastExact>{});
+#pragma unroll
+        for (int qh = 0; qh < kQH; ++qh) l_tot[qh] = sum_across_groups(l_run[qh]);
+      }
+    } else {
+      key_loop(std::integral_constant<int, kPassFast>{});
+#pragma unroll
+      for (int qh = 0; qh < kQH; ++qh) l_tot[qh] = lsum[qh][0];
+    }
     bool overflow = false;
 #pragma unroll
-    for (int qh = 0; qh < kQH; ++qh) {
-      l_tot[qh] = lsum[qh][0];
+    for (int qh = 0; qh < kQH; ++qh)
       overflow |= !(l_tot[qh] <= kFastLimit);   // (a NaN sum counts as an overflow)
-    }
     // One flag per wave through LDS (the tiles are no longer read after the
     // first barrier; the last one keeps the flags from being overwritten by
     // the checked pass's copies before every wave has read them).
@@ -704,10 +724,12 @@ void attn_bf16_kernel(const __bf16* __restrict__ q, __bf16* __restrict__ out, in
       for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
         for (int qh = 0; qh < kQH; ++qh) o[dt][qh] = f32x4{};
+#pragma unroll
+      for (int qh = 0; qh < kQH; ++qh) l_run[qh] = 0.0f;
     }
   }
   if (checked_pass) {
-    key_loop(std::true_type{});
+    key_loop(std::integral_constant<int, kPassChecked>{});
 #pragma unroll
     for (int qh = 0; qh < kQH; ++qh) l_tot[qh] = sum_across_groups(l_run[qh]);
   }
