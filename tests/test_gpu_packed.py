@@ -137,6 +137,40 @@ def test_packed_equals_sequential_ring(dtype, d):
         assert np.abs(gp - gs).max() <= 1e-5
 
 
+@pytest.mark.parametrize("d", [128, 64])
+def test_packed_log_sum_exp_reference_far_below_the_max(d):
+    """The launch that also writes the log-sum-exp (the training forward) when a
+    chunk's first block sets a reference far below its largest scores: chunk 0's
+    keys are tiny and the first block of every chunk's read set is chunk 0's;
+    keys scaled by 8 give probabilities up to ~2^35 relative to that reference,
+    keys scaled by 24 push row sums past 2^64, so the units of chunks 3 and 4
+    run the checked pass after the fast one.  Output and base-2 log-sum-exp
+    against the oracle (log2_sum_exp2 over the packed mask)."""
+    n, W = 5, 4
+    w = small("bf16", d, grid=(6, 11), ring_chunks=W, n_chunks=n)
+    q, k, v = clip(w, n)
+    Nq = w.chunk_tokens
+    factors = [0.01, 8.0, 8.0, 24.0, 1.0]
+    k = torch.cat([(k[c * Nq:(c + 1) * Nq].float() * f).to(torch.bfloat16)
+                   for c, f in enumerate(factors)])
+    q, k, v = to_dev(q), to_dev(k), to_dev(v)
+    scale = 1.0 / math.sqrt(d)
+    lse = torch.empty((n * Nq, w.heads), dtype=torch.float32, device=q.device)
+    out = ff.packed_attention(q, k, v, n_chunks=n, window=W, anchor_k=None, anchor_v=None,
+                              frame_tokens=w.tokens_per_frame, anchors_of_chunk=None,
+                              scale=scale, lse=lse)
+    torch.cuda.synchronize()
+    ref = oracle_packed(w, q, k, v, None, None, None, W, scale)
+    got = exact(out)
+    for c in range(n):
+        check_attention(got[c * Nq:(c + 1) * Nq], ref[c], "bf16",
+                        f"chunk {c} (key scale {factors[c]:g})")
+    M = fo.packed_visibility(n, Nq, w.tokens_per_frame, 0, [[]] * n, W)
+    rlse = fo.log2_sum_exp2(exact(q), exact(k), M, scale)
+    err = float(np.abs(exact(lse) - rlse).max())
+    assert err <= 2e-3, f"log-sum-exp off by {err:.2e} (log2 units)"
+
+
 @pytest.mark.parametrize("name", ["1.3b-480p", "14b-720p"])
 def test_packed_full_size_sampled_rows(name):
     """A whole clip of one stage (27 chunks, W = 4, anchor windows Gamma(i)) at
