@@ -114,6 +114,85 @@ def test_backward_frame_seen_by_several_chunk_runs():
     run_case(6, 130, 64, 2, table, 1, 2, 128, seed=5)
 
 
+def test_backward_14b_720p_sampled():
+    """The shape the benchmark times: 14B 720p clip (27 chunks x 10800 tokens, 40
+    heads x 128, W = 4, Gamma(i) windows from the 9-frame bank).  dO is zero
+    except on sampled rows R of chunks 24-26 (both ends of the chunk, its middle,
+    the ragged last tile); every other row then has dP = 0 and D = 0, so dS = 0
+    and it adds exactly nothing, while the kernels still stream every query tile
+    of every key unit.  Checked for one head against the oracle's float64
+    gradient (oracle.masked_attention_grad) of each query chunk over its visible
+    set, on the rows R only: dQ and the log-sum-exp of R, dK and dV of sampled
+    keys of chunk 24 (seen by chunks 24-26) and of an anchor frame of chunk 24
+    (seen by every chunk whose window lists it)."""
+    w = synth.WORKLOADS["14b-720p"]
+    n, W, Nq, G, h, d = w.n_chunks, w.ring_chunks, w.chunk_tokens, w.tokens_per_frame, w.heads, w.head_dim
+    dev = torch.device("cuda", 0)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(21)
+    rnd = lambda shape: torch.randn(shape, generator=gen, device=dev).to(torch.bfloat16)
+    q, k, v = (rnd((n * Nq, h, d)) for _ in range(3))
+    frames = sorted({f for c in range(n) for f in anchor_frames(w, c)})
+    ak, av = rnd((len(frames) * G, h, d)), rnd((len(frames) * G, h, d))
+    table = [[frames.index(f) for f in anchor_frames(w, c)] for c in range(n)]
+    c = n - 3
+    chunks_r = [c, c + 1, c + 2]
+    rows = np.concatenate([np.arange(0, 64), np.arange(5000, 5032), np.arange(Nq - 40, Nq)])
+    sel = np.concatenate([i * Nq + rows for i in chunks_r])
+    dout = torch.zeros((n * Nq, h, d), dtype=torch.bfloat16, device=dev)
+    dout[torch.as_tensor(sel, device=dev)] = rnd((len(sel), h, d))
+    scale = 1.0 / math.sqrt(d)
+    lse = torch.empty((n * Nq, h), dtype=torch.float32, device=dev)
+    out = ff.packed_attention(q, k, v, n_chunks=n, window=W, anchor_k=ak, anchor_v=av,
+                              frame_tokens=G, anchors_of_chunk=table, scale=scale, lse=lse)
+    dq, dk, dv, dak, dav = ff.packed_attention_bwd(q, k, v, out, dout, lse, n_chunks=n, window=W,
+                                                   anchor_k=ak, anchor_v=av, frame_tokens=G,
+                                                   anchors_of_chunk=table, scale=scale)
+    torch.cuda.synchronize()
+    for t in (dq, dk, dv, dak, dav):
+        assert torch.isfinite(t.float()).all()
+    hd = 17
+    one = lambda x: exact(x)[:, None, :]          # [tokens][1 head][d] for the oracle
+    fa = table[c][-1]                              # an anchor frame chunk c sees
+
+    def visible(i):
+        """K, V of chunk i's visible set for head hd, and where chunk c's keys
+        and frame fa's keys start in it (None where absent)."""
+        ks = [ak[f * G:(f + 1) * G, hd] for f in table[i]]
+        vs = [av[f * G:(f + 1) * G, hd] for f in table[i]]
+        first = max(0, i - W)
+        ks.append(k[first * Nq:(i + 1) * Nq, hd])
+        vs.append(v[first * Nq:(i + 1) * Nq, hd])
+        at_c = len(table[i]) * G + (c - first) * Nq if first <= c <= i else None
+        at_fa = table[i].index(fa) * G if fa in table[i] else None
+        return one(torch.cat(ks)), one(torch.cat(vs)), at_c, at_fa
+
+    key_tok = np.arange(100, 164)
+    anc_tok = np.arange(200, 264)
+    gk, gv = np.zeros((len(key_tok), d)), np.zeros((len(key_tok), d))
+    ga_k, ga_v = np.zeros((len(anc_tok), d)), np.zeros((len(anc_tok), d))
+    for i in chunks_r:
+        Ki, Vi, at_c, at_fa = visible(i)
+        Qr, dOr = one(q[i * Nq + rows, hd]), one(dout[i * Nq + rows, hd])
+        allv = np.ones((len(rows), Ki.shape[0]), bool)
+        dq_ref, dK_ref, dV_ref = fo.masked_attention_grad(Qr, Ki, Vi, allv, dOr, scale)
+        check_grad(exact(dq[i * Nq + rows, hd]), dq_ref[:, 0], f"dq rows of chunk {i}")
+        lse_ref = fo.log2_sum_exp2(Qr, Ki, allv, scale)[:, 0]
+        assert float(np.abs(exact(lse[i * Nq + rows, hd]) - lse_ref).max()) <= LSE_ABS
+        if at_c is not None:
+            gk += dK_ref[at_c + key_tok, 0]
+            gv += dV_ref[at_c + key_tok, 0]
+        if at_fa is not None:
+            ga_k += dK_ref[at_fa + anc_tok, 0]
+            ga_v += dV_ref[at_fa + anc_tok, 0]
+    check_grad(exact(dk[c * Nq + key_tok, hd]), gk, "dk keys")
+    check_grad(exact(dv[c * Nq + key_tok, hd]), gv, "dv keys")
+    check_grad(exact(dak[fa * G + anc_tok, hd]), ga_k, "d_anchor_k keys")
+    check_grad(exact(dav[fa * G + anc_tok, hd]), ga_v, "d_anchor_v keys")
+    # rows outside R add nothing: keys of a chunk no row of R sees have zero gradients
+    assert float(np.abs(exact(dk[(c - W - 1) * Nq:(c - W) * Nq, hd])).max()) == 0.0
+
+
 def test_backward_full_clip_sampled():
     """1.3B 480p clip (27 chunks x 4680 tokens, 12 heads x 128, W = 4, Gamma(i)
     windows from a 9-frame bank): one backward, checked against the oracle's
