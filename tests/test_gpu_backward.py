@@ -102,6 +102,13 @@ def test_backward_peaked_softmax(d):
     run_case(6, 198, 66, 3, TABLE6, 2, 2, d, seed=13, key_scale=6.0)
 
 
+@pytest.mark.parametrize("d", [128, 64])
+def test_backward_one_token_chunks(d):
+    # 1-token chunks and 1-token anchor frames: every streamed tile holds one
+    # valid row, every key unit one valid key
+    run_case(5, 1, 1, 2, [[0], [], [1, 0], [1], []], 2, 2, d, seed=17)
+
+
 def test_backward_multi_tile_and_hidden_frame():
     # 288-token chunks (4.5 tiles), 96-token frames, a frame no chunk lists, 4 heads
     table = [[0], [0, 1], [1], [1, 3], [3], [3]]

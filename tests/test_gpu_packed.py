@@ -95,6 +95,9 @@ def test_packed_single_chunk_and_short_chunks():
     run_and_check(w, 1, 3, [[0]], 1)
     w2 = small("bf16", 64, grid=(3, 6), frames_per_chunk=1)
     run_and_check(w2, 5, 2, [[0], [], [0], [0], []], 1)
+    # 1-token chunks and 1-token anchor frames (a 1x1 grid)
+    w3 = small("bf16", 128, grid=(1, 1), frames_per_chunk=1)
+    run_and_check(w3, 5, 2, [[0], [], [1, 0], [1], []], 2)
 
 
 @pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])

@@ -204,6 +204,22 @@ def test_attention_degenerate_shapes():
         run.step(c, 0, 0)
 
 
+@pytest.mark.parametrize("dtype,head_dim", [("bf16", 128), ("bf16", 64), ("f32", 64)])
+def test_attention_one_token_chunks(dtype, head_dim):
+    # The most degenerate shape: a 1x1 latent grid and 1-frame chunks, so every
+    # chunk, history chunk and anchor frame is one token (each segment one valid
+    # key, the second 32-key block of every tile fully masked); anchors at
+    # latent frames 0 and 3, a ring of 2, two stages, RoPE included.
+    w = synth.small_workload("one-token", dtype=dtype, heads=2, head_dim=head_dim, grid_h=1,
+                             grid_w=1, frames_per_chunk=1, ring_chunks=2, stages=2, layers=1,
+                             n_chunks=6, anchor_rule="fixed:0,3", max_anchor_frames=2, wid=102)
+    run = PairedRun(w)
+    for c in range(w.n_chunks):
+        for s in range(w.stages):
+            run.step(c, s, 0)
+    assert len(run.results) == w.n_chunks * w.stages
+
+
 @pytest.mark.parametrize("head_dim", [64, 128])
 @pytest.mark.parametrize("grid", [(6, 11), (12, 22)])
 def test_attention_tail_split_into_key_parts(head_dim, grid):
