@@ -215,6 +215,19 @@ def test_static_backward_rejects_inputs_beyond_its_scratch():
     assert "static scratch" in L.ff_last_error().decode()
     assert call(packed_desc(dtype=ff.FF_DT_F32)) == 5                 # bf16 only, as the other entry
     assert call(packed_desc(head_dim=96)) == 5
+    # the backward's per-frame tables: at most 64 anchor frames, each seen by at
+    # most 8 runs of consecutive chunks
+    def call_anchors(d):
+        return L.ff_packed_attention_bwd_static(ctypes.byref(d), FAKE_DEV, FAKE_DEV, FAKE_DEV,
+                                                FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV, lse, FAKE_DEV,
+                                                FAKE_DEV, FAKE_DEV, FAKE_DEV, FAKE_DEV,
+                                                ctypes.c_float(0.125), None)
+    arr, ptr = table([[0]] * 6)
+    assert call_anchors(packed_desc(n_anchor_frames=65, anchors_of_chunk=ptr)) == 5
+    assert "64 anchor frames" in L.ff_last_error().decode()
+    arr9, ptr9 = table([[0] if c % 2 == 0 else [] for c in range(18)])   # 9 runs of frame 0
+    assert call_anchors(packed_desc(n_chunks=18, n_anchor_frames=1, anchors_of_chunk=ptr9)) == 5
+    assert "more than 8 runs" in L.ff_last_error().decode()
 
 
 # ----------------------------------------------------------------------

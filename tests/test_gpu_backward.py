@@ -102,6 +102,17 @@ def test_backward_peaked_softmax(d):
     run_case(6, 198, 66, 3, TABLE6, 2, 2, d, seed=13, key_scale=6.0)
 
 
+def test_backward_largest_launch_shape():
+    # 128 chunks (the most one packed launch takes), W = 8, 2-token chunks and
+    # 1-token anchor frames; chunk c lists frames c // 16 and c // 16 + 1, so
+    # frame f is seen by one run of chunks and, through chunk 127's table of
+    # eight frames, by a second one
+    n = 128
+    tab = [[c // 16, c // 16 + 1] for c in range(n)]
+    tab[127] = list(range(1, 9))
+    run_case(n, 2, 1, 9, tab, 8, 2, 64, seed=19)
+
+
 @pytest.mark.parametrize("d", [128, 64])
 def test_backward_one_token_chunks(d):
     # 1-token chunks and 1-token anchor frames: every streamed tile holds one

@@ -100,6 +100,18 @@ def test_packed_single_chunk_and_short_chunks():
     run_and_check(w3, 5, 2, [[0], [], [1, 0], [1], []], 2)
 
 
+def test_packed_largest_launch_shape():
+    # FF_MAX_PACKED_CHUNKS = 128 chunks in one launch, the widest window W = 8,
+    # 2-token chunks and 1-token anchor frames from a bank of 9; chunk c lists
+    # frames c // 16 .. c // 16 + c % 3 (1-3 frames, each frame seen by one run
+    # of chunks) and chunk 127 all eight frames it can list
+    w = small("bf16", 64, grid=(1, 2), frames_per_chunk=1)
+    n = 128
+    tab = [[f for f in range(c // 16, min(9, c // 16 + c % 3 + 1))] for c in range(n)]
+    tab[127] = list(range(1, 9))
+    run_and_check(w, n, 8, tab, 9)
+
+
 @pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
 def test_packed_equals_sequential_ring(dtype, d):
     """Chunk i of the packed launch against ff_chunk_attention of chunk i after
