@@ -218,12 +218,18 @@ __device__ __attribute__((always_inline)) inline void run_ring(int n, int wave, 
   } else if (wave < R::kCopyWaves) {
     issue(s0);
     if (R::kAhead > 1 && n > 1) issue(s1);
+    // With two tiles ahead the copies go out after the step's blocks (what the
+    // blocks reload from scratch then waits only for older copies); with one,
+    // before them (the copy needs the whole step to land).
     auto step = [&](int t, char* cur, char* ahead) __attribute__((always_inline)) {
       copy_sync(t);
-      if (t + R::kAhead < n) issue(ahead);
+      if constexpr (R::kAhead < 2)
+        if (t + R::kAhead < n) issue(ahead);
       const int nv = next_nv();
       block(cur, 0, nv);
       if constexpr (kBlocks == 2) block(cur, 1, nv);
+      if constexpr (R::kAhead >= 2)
+        if (t + R::kAhead < n) issue(ahead);
     };
     for (int t = 0; t < n;) {
       if constexpr (NS == 3) {
