@@ -69,7 +69,8 @@ struct Cfg {
 
 // Ring schedules.  NS = 2: all eight waves copy tile t+1 after barrier t and
 // then work on tile t in lock step.  NS >= 3: waves 0-3 copy tile t + NS - 2
-// after barrier t and run both 32-row blocks of tile t; their SIMD partners,
+// after barrier t (before their blocks with three slots, after them with
+// four) and run both 32-row blocks of tile t; their SIMD partners,
 // waves 4-7, run block 1 of tile t-1 and then block 0 of tile t, half a tile
 // later, so one wave's exponentials meet the other's matrix work.  Tile u
 // sits in slot u % NS; its last reads (block 1 by waves 4-7) precede barrier
@@ -100,8 +101,8 @@ __device__ inline uint64_t readlane_u64(uint64_t v, int lane) {
   return (uint64_t(hi) << 32) | uint64_t(lo);
 }
 
-// Streams the tiles of up to kMaxRuns runs of rows through a two-slot LDS
-// ring.  Run i (held by lane i, read with v_readlane): `len` rows of two
+// Streams the tiles of up to kMaxRuns runs of rows through an LDS ring of
+// two to four slots.  Run i (held by lane i, read with v_readlane): `len` rows of two
 // token-major tensors (row r at a + r * row_bytes and b + r * row_bytes, this
 // head's columns) and, with kVec, two float vectors (element r at
 // va + r * vec_bytes and vb + r * vec_bytes).
